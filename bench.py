@@ -1,0 +1,243 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused PHub exchange step on one MI355X.
+
+One step = every worker pushes all its keys (pointer registration) and the
+job runs one fused aggregate + optimize launch over all keys, for every job
+of the workload.  Gradients, weights and momentum are resident in HBM before
+the timed region starts.  Prints one JSON line:
+
+  metric   worker-gradient GB/s aggregated+optimized per step
+  value    N * P * 4 bytes per step / wall time per step, summed over jobs
+  roofline the fused kernel's algorithmic HBM bytes ((N + 4) * P * 4 per
+           launch) / its average launch duration, measured with HIP events on
+           the job's stream, against the 8 TB/s HBM3E peak
+  cpu_baseline the CPU oracle timed on the host over a bounded sample
+
+Usage: python bench.py [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCES = ["paper_1805_07891_amd/csrc/fused_step.hip", "paper_1805_07891_amd/csrc/kernels.hpp"]
+DEFAULT_WORKLOAD = "resnet50"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the kernel as it is now (same source hash); else None."""
+    path = os.path.join(ROOT, "profiles", f"fused_step_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, grads_dev, w0_dev, budget_s: float):
+    """The oracle on the host, single-threaded, over the workload's first job
+    (all keys) or a prefix of its keys, until `budget_s` seconds of work."""
+    import numpy as np
+    import oracle
+    spec = wl.jobs[0]
+    # bound host memory: take a prefix of keys with at most ~2 GB of inputs
+    limit = 2e9 / ((spec.num_workers + 2) * 4)
+    nkeys, acc = 0, 0
+    for n in spec.key_elems:
+        if acc + n > limit and nkeys > 0:
+            break
+        acc += n
+        nkeys += 1
+    from paper_1805_07891_amd.workloads import key_offsets
+    offs, _ = key_offsets(spec.key_elems)
+    g_host = [grads_dev[w].cpu().numpy() for w in range(spec.num_workers)]
+    w_host = w0_dev.cpu().numpy()
+    grads = [[g[o:o + n] for o, n in zip(offs[:nkeys], spec.key_elems[:nkeys])] for g in g_host]
+    W = [w_host[o:o + n].copy() for o, n in zip(offs[:nkeys], spec.key_elems[:nkeys])]
+    M = [np.zeros(n, np.float32) for n in spec.key_elems[:nkeys]]
+    try:
+        cores = os.sched_getaffinity(0)
+        os.sched_setaffinity(0, {min(cores)})
+    except (AttributeError, OSError):
+        cores = None
+    steps, t0 = 0, time.perf_counter()
+    try:
+        while True:
+            oracle.step(grads, W, M, spec.lr, spec.momentum, spec.weight_decay, spec.nesterov)
+            steps += 1
+            if time.perf_counter() - t0 >= budget_s:
+                break
+    finally:
+        if cores is not None:
+            os.sched_setaffinity(0, cores)
+    dt = time.perf_counter() - t0
+    params = sum(spec.key_elems[:nkeys])
+    return {
+        "value": round(spec.num_workers * params * 4 * steps / dt / 1e9, 3),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{spec.name}: {nkeys} of {spec.num_keys} keys ({params:,} of "
+                   f"{spec.num_params:,} params), N={spec.num_workers}, {steps} steps in "
+                   f"{dt:.1f} s, one thread pinned to one core"),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="budget of the CPU oracle baseline (0 skips it)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 512 MiB device copy three times (a known-size "
+                         "reference for hardware byte counters)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the exchange step here runs on a single "
+              f"MI355X with all workers simulated in its HBM; --gpus {args.gpus} is not "
+              f"supported.", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_1805_07891_amd import workloads
+    from paper_1805_07891_amd.job import TorchJob, load_library
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    lib = load_library()
+    wl = workloads.workload(args.workload)
+
+    if args.copy_calibration:
+        src = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    jobs, grads, w0s = [], [], []
+    for ji, spec in enumerate(wl.jobs):
+        stream = torch.cuda.Stream(device=dev)
+        job = TorchJob(spec, dev, stream=stream, lib=lib)
+        w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
+        g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
+             for w in range(spec.num_workers)]
+        torch.cuda.synchronize()
+        job.set_weights(w0)
+        for w, a in enumerate(g):
+            job.attach_grads(w, a)
+        jobs.append(job)
+        grads.append(g)
+        w0s.append(w0)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        for job in jobs:
+            job.push_and_step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(K)] for _ in jobs]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(K):
+        for j, job in enumerate(jobs):
+            job.push_all()
+            ev[j][s][0].record(job.stream)
+            job.step()
+            ev[j][s][1].record(job.stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    ms_per_step = (t1 - t0) * 1e3 / K
+    worker_bytes = wl.worker_grad_bytes_per_step()
+    value = worker_bytes / (ms_per_step * 1e-3) / 1e9
+    whole_hbm = wl.hbm_bytes_per_step() / (ms_per_step * 1e-3) / 1e9
+
+    # dominant kernel: the job with the most bytes per launch
+    dom = max(range(len(jobs)), key=lambda j: wl.jobs[j].hbm_bytes_per_step())
+    durs = [ev[dom][s][0].elapsed_time(ev[dom][s][1]) for s in range(K)]
+    avg_ms = sum(durs) / len(durs)
+    dom_bytes = wl.jobs[dom].hbm_bytes_per_step()
+    achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
+    traffic = measured_traffic(args.workload)
+    groups, threads, segs = jobs[dom].info()
+
+    baseline = None
+    if args.cpu_seconds > 0:
+        baseline = cpu_baseline(wl, grads[0], w0s[0], args.cpu_seconds)
+
+    out = {
+        "metric": "worker-gradient GB/s aggregated+optimized per step; % of HBM peak",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "jobs": [{"name": j.name, "workers": j.num_workers, "keys": j.num_keys,
+                      "params": j.num_params} for j in wl.jobs],
+            "chunk_bytes": wl.jobs[0].chunk_bytes,
+            "optimizer": {"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
+                          "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov},
+            "hbm_bytes_per_step": wl.hbm_bytes_per_step(),
+            "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
+            "launch": {"workgroups": groups, "threads": threads, "segments": segs},
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "fused_step_fixed" if wl.jobs[dom].num_workers <= 16 else "fused_step_any",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "avg_launch_us": round(avg_ms * 1e3, 2),
+            "algorithmic_bytes_per_launch": dom_bytes,
+            "kernel_source_hash": kernel_source_hash(),
+        },
+        "cpu_baseline": baseline,
+    }
+    print(json.dumps(out), flush=True)
+    for job in jobs:
+        job.destroy()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

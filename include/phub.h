@@ -1,0 +1,227 @@
+/*
+ * phub.h - C interface of the PHub gradient-exchange step on one MI355X GPU.
+ *
+ * The paper (Parameter Hub, section 3.1) states the service as: create a
+ * job handle and namespace, initialise receive and merge buffers, then let
+ * workers Push gradients for keys and Pull the updated model.  Between push
+ * and pull the server aggregates every key's gradients over all workers and
+ * runs the optimizer on the result (section 3.2.2), chunk by chunk (section
+ * 3.2.3), with chunks mapped to cores by a schedule fixed at initialisation
+ * (section 3.2.4).
+ *
+ * Here the server is one GPU.  The N workers' gradients are device buffers
+ * that the caller owns; a push registers a pointer and copies nothing.  One
+ * step runs one fused kernel over all keys: it sums the N gradients of each
+ * element in ascending worker order in fp32 and applies momentum or
+ * Nesterov SGD with coupled weight decay to the job's master weights and
+ * momentum, reading each gradient byte once.
+ *
+ * Per element, with s the sum, w the weight and m the momentum, each line a
+ * single fused multiply-add rounded once to fp32:
+ *     d  = wd * w + s
+ *     m' = mu * m + d
+ *     u  = mu * m' + d     (Nesterov)   or   u = m'   (plain momentum)
+ *     w' = -lr * u + w
+ *
+ * Conventions for every function below:
+ *   - the return value is PHUB_OK (0) or a negative PHUB_E* code; no
+ *     exception or signal crosses this interface;
+ *   - on an error nothing is enqueued or changed, and phub_last_error()
+ *     returns a message for the calling thread;
+ *   - "device pointer" means memory of the GPU that was current when the job
+ *     was created (torch tensors' data_ptr(), hipMalloc memory);
+ *   - calls on one job must not overlap; different jobs may be driven from
+ *     different threads.
+ */
+#ifndef PHUB_H
+#define PHUB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum phub_status {
+    PHUB_OK = 0,
+    PHUB_EINVAL = -1,    /* an argument is out of range, null or misaligned */
+    PHUB_ENOTREADY = -2, /* phub_step before every (worker, key) was pushed */
+    PHUB_ENOMEM = -3,    /* device or host allocation failed */
+    PHUB_EHIP = -4,      /* a HIP runtime call failed (message names it) */
+    PHUB_ESTATE = -5     /* the handle is not a live job */
+};
+
+/* One training job: a namespace of keys, its workers, master weights and
+ * momentum (the handle of section 3.1).  Opaque. */
+typedef struct phub_job phub_job;
+
+/*
+ * phub_init - create a job (section 3.1: CreateService + InitService).
+ *   out           receives the new handle.
+ *   num_workers   N, 1 <= N <= 4096: the number of gradients summed per key.
+ *   num_keys      K >= 1: the number of keys (one layer's parameters each,
+ *                 section 2).
+ *   key_elems     host array of K element counts, each 0 <= n_k < 2^40.
+ *   chunk_bytes   size of the chunks keys are split into for scheduling
+ *                 (section 3.2.3; the paper's default is 32768); a positive
+ *                 multiple of 16, at most 2^30.  Results do not depend on it.
+ *   lr, momentum, weight_decay
+ *                 optimizer settings (section 4.2), finite fp32 values, kept
+ *                 for the life of the job.
+ *   nesterov      nonzero for Nesterov momentum, zero for plain momentum.
+ *   hip_stream    the hipStream_t all of the job's device work is ordered
+ *                 on, or NULL to let the job create its own non-blocking
+ *                 stream (destroyed with the job).  A caller's stream is
+ *                 borrowed and must outlive the job.
+ * The job allocates its master weights W and momentum M (fp32, each key's
+ * slice 256-byte aligned), sets both to zero, computes the chunk schedule
+ * (section 3.2.4) and uploads it.  Errors: PHUB_EINVAL, PHUB_ENOMEM,
+ * PHUB_EHIP.  On error *out is set to NULL.
+ */
+int phub_init(phub_job **out, int num_workers, int num_keys, const int64_t *key_elems,
+              int64_t chunk_bytes, float lr, float momentum, float weight_decay,
+              int nesterov, void *hip_stream);
+
+/*
+ * phub_set_weights - load key `key`'s master weights from `src` (n_k fp32
+ * values, device or host memory) and reset its momentum to zero.  The copy
+ * is ordered on the job's stream; `src` must stay valid until it has run
+ * (phub_sync).  Errors: PHUB_EINVAL, PHUB_ESTATE, PHUB_EHIP.
+ */
+int phub_set_weights(phub_job *job, int key, const float *src);
+
+/*
+ * phub_push - worker `worker` pushes its gradient for key `key` (section
+ * 3.1 Push; zero-copy registration as in section 3.2.1).
+ *   grad   device pointer to n_k fp32 values, 16-byte aligned (may be NULL
+ *          only when n_k == 0).  The caller keeps ownership; the buffer must
+ *          stay valid and unchanged until the step that consumes it has run
+ *          on the job's stream.
+ * Nothing is copied: the pointer is recorded for the next phub_step.  The
+ * worker index, not the call order, fixes the worker's place in the sum.
+ * Pushing a pair again before the step replaces the earlier pointer.
+ * Errors: PHUB_EINVAL (range, null, alignment), PHUB_ESTATE.
+ */
+int phub_push(phub_job *job, int worker, int key, const float *grad);
+
+/*
+ * phub_push_keys - batched phub_push for one worker: pushes grads[i] for key
+ * keys[i], i < count (keys == NULL means keys 0 .. count-1).  Same rules as
+ * phub_push; either every pointer is recorded or, on error, none is.
+ */
+int phub_push_keys(phub_job *job, int worker, int count, const int *keys,
+                   const float *const *grads);
+
+/*
+ * phub_step - aggregate and optimize every key (sections 3.2.2-3.2.4): one
+ * kernel launch over all keys on the job's stream, asynchronous to the
+ * host.  Requires every (worker, key) pair to have been pushed since the
+ * previous step, else PHUB_ENOTREADY and nothing is enqueued.  If a pushed
+ * pointer differs from the last step's, the pointer table is uploaded on the
+ * same stream first.  Afterwards all pairs count as not pushed.
+ * Errors: PHUB_ENOTREADY, PHUB_ESTATE, PHUB_EHIP.
+ */
+int phub_step(phub_job *job);
+
+/*
+ * phub_pull - the current master weights of key `key` (section 3.1 Pull):
+ * *weights receives a device pointer to n_k fp32 values owned by the job.
+ * Reads are ordered after earlier steps on the job's stream (phub_sync
+ * before reading from another stream or the host); the values change at the
+ * next phub_step and the pointer is valid until phub_destroy.
+ * Errors: PHUB_EINVAL, PHUB_ESTATE.
+ */
+int phub_pull(phub_job *job, int key, const float **weights);
+
+/*
+ * phub_get_state - device pointers to key `key`'s master weights and
+ * momentum (n_k fp32 each, job-owned, same validity as phub_pull).  Either
+ * output may be NULL.  Errors: PHUB_EINVAL, PHUB_ESTATE.
+ */
+int phub_get_state(phub_job *job, int key, const float **weights, const float **momentum);
+
+/*
+ * phub_sync - wait on the host until all work enqueued by the job has run.
+ * Errors: PHUB_ESTATE, PHUB_EHIP (including faults of earlier launches).
+ */
+int phub_sync(phub_job *job);
+
+/*
+ * phub_get_stream - the hipStream_t the job orders its work on.
+ */
+int phub_get_stream(phub_job *job, void **hip_stream);
+
+/*
+ * phub_job_info - launch shape of the job's step: the number of workgroups
+ * of one launch, the threads per workgroup and the number of work segments
+ * in the schedule.  Any output may be NULL.
+ */
+int phub_job_info(phub_job *job, int *workgroups, int *threads_per_group, int64_t *segments);
+
+/*
+ * phub_destroy - wait for the job's work, free its memory (W, M, schedule,
+ * pointer table) and its own stream.  The handle is dead afterwards; passing
+ * it again to any function returns PHUB_ESTATE.
+ */
+int phub_destroy(phub_job *job);
+
+/* Message of the last failed call on this thread ("" if none).  The string
+ * belongs to the library and lives until the thread's next failing call. */
+const char *phub_last_error(void);
+
+/* --------------------------------------------------------------------------
+ * The chunk schedule (section 3.2.4), computed on the host only.  phub_init
+ * runs it; it is exported so that its coverage and balance can be checked
+ * without a GPU.
+ *
+ * Keys are cut into chunks of chunk_bytes/4 elements, the last one partial
+ * (section 3.2.3's virtual keys).  Keys smaller than a chunk are bundled, in
+ * key order, into items of at most one chunk (a run of small keys is not
+ * bundled across a larger key).  While there are fewer than min_items
+ * items, the chunk is halved (not below 1024 elements) so that every
+ * compute unit gets work; the result of a step does not depend on the cut.
+ * Items are assigned to at most num_groups workgroups by the
+ * longest-processing-time-first rule (largest item first, each to the least
+ * loaded workgroup, lowest index on ties), a 4/3-approximate balanced
+ * partition like the paper's (section 3.2.4).  Item cost is the bytes it
+ * moves, (N + 4) * 4 per element, plus 4096 per segment.  With num_groups
+ * at least the number of items, workgroup g holds the g-th largest item,
+ * and the GPU's in-order dispatch of workgroups performs the same rule
+ * online.
+ * ------------------------------------------------------------------------ */
+
+/* One contiguous run of one key handled by one workgroup. */
+typedef struct phub_segment {
+    int32_t key;    /* key index */
+    int32_t count;  /* number of elements, >= 1 */
+    int64_t offset; /* index of the first element within the key */
+} phub_segment;
+
+/*
+ * phub_plan_count - sizes of the schedule for these arguments (same meaning
+ * and checks as phub_init; num_groups >= 1 caps the workgroups, min_items
+ * >= 0 is the refinement target above): *num_segments and *groups_used
+ * (<= num_groups; workgroups with no work are dropped), and *item_elems
+ * (may be NULL), the chunk size after refinement.  Errors: PHUB_EINVAL.
+ */
+int phub_plan_count(int num_workers, int num_keys, const int64_t *key_elems,
+                    int64_t chunk_bytes, int num_groups, int min_items,
+                    int64_t *num_segments, int *groups_used, int64_t *item_elems);
+
+/*
+ * phub_plan_build - the schedule itself, into caller arrays sized by
+ * phub_plan_count: segments[num_segments], grouped by workgroup;
+ * group_begin[groups_used + 1] with workgroup g owning segments
+ * group_begin[g] .. group_begin[g+1]-1 (in key, then offset, order);
+ * group_cost[groups_used] (may be NULL) the cost assigned to each workgroup.
+ * Errors: PHUB_EINVAL.
+ */
+int phub_plan_build(int num_workers, int num_keys, const int64_t *key_elems,
+                    int64_t chunk_bytes, int num_groups, int min_items,
+                    phub_segment *segments, int64_t *group_begin, int64_t *group_cost);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PHUB_H */

@@ -1,0 +1,500 @@
+// C interface of the exchange step: job state, push/step/pull, schedule.
+//
+// The paper's service (section 3.1) creates a job with its own namespace and
+// buffers, then serves Push and Pull.  A job here owns its master weights W
+// and momentum M in HBM, the schedule computed at creation (section 3.2.4),
+// a device copy of the (worker, key) -> gradient pointer table, and the
+// stream its work is ordered on.  A push only records a pointer (the
+// zero-copy registration of section 3.2.1); a step uploads the pointer table
+// if it changed and launches one fused kernel for all keys.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "kernels.hpp"
+#include "phub.h"
+#include "plan.hpp"
+
+#ifndef PHUB_BLOCK_THREADS
+#define PHUB_BLOCK_THREADS 256
+#endif
+// Cap on workgroups per compute unit in the schedule; 0 means one workgroup
+// per item (the dispatcher then runs the items largest first).
+#ifndef PHUB_GROUPS_PER_CU
+#define PHUB_GROUPS_PER_CU 0
+#endif
+
+static_assert(PHUB_BLOCK_THREADS >= 64 && PHUB_BLOCK_THREADS <= phub::kMaxBlockThreads &&
+                  PHUB_BLOCK_THREADS % 64 == 0,
+              "block size must be a multiple of the wave size");
+
+namespace {
+
+constexpr int kStageSlots = 4;       // pinned staging buffers for pointer-table uploads
+constexpr int64_t kArenaAlign = 64;  // elements: 256-byte aligned key slices
+
+thread_local std::string g_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(PHUB_EHIP, "%s failed: %s (%d)", what, hipGetErrorString(e), int(e));
+}
+
+std::mutex g_live_mu;
+std::unordered_set<const void*> g_live;
+
+}  // namespace
+
+struct phub_job {
+    int num_workers = 0;
+    int num_keys = 0;
+    std::vector<int64_t> key_elems;
+    std::vector<int64_t> arena_offset;  // per key, elements
+    int64_t arena_elems = 0;
+    int64_t chunk_bytes = 0;
+    float lr = 0, mu = 0, wd = 0;
+    bool nesterov = false;
+
+    int device = 0;
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+
+    int groups = 0;
+    int block = PHUB_BLOCK_THREADS;
+    int64_t num_segments = 0;
+
+    float* weights = nullptr;
+    float* moments = nullptr;
+    phub::DevSegment* d_segments = nullptr;
+    int64_t* d_group_begin = nullptr;
+    const float** d_grads = nullptr;
+
+    std::vector<const float*> grads;  // host table, [key * N + worker]
+    std::vector<uint8_t> pushed;      // same layout: pushed since the last step
+    int64_t num_pushed = 0;
+    bool table_dirty = true;          // host table differs from the device copy
+
+    const float** stage[kStageSlots] = {};
+    hipEvent_t stage_done[kStageSlots] = {};
+    bool stage_used[kStageSlots] = {};
+    int stage_next = 0;
+};
+
+namespace {
+
+// Makes the job's device current for the duration of a call.
+class DeviceScope {
+  public:
+    explicit DeviceScope(int device) {
+        if (hipGetDevice(&prev_) != hipSuccess) prev_ = -1;
+        if (prev_ != device) ok_ = hipSetDevice(device) == hipSuccess;
+    }
+    ~DeviceScope() {
+        int cur = -1;
+        if (prev_ >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev_) (void)hipSetDevice(prev_);
+    }
+    bool ok() const { return ok_; }
+
+  private:
+    int prev_ = -1;
+    bool ok_ = true;
+};
+
+bool is_live(const phub_job* j) {
+    std::lock_guard<std::mutex> lk(g_live_mu);
+    return j && g_live.count(j) != 0;
+}
+
+void release(phub_job* j) {
+    if (j->d_grads) (void)hipFree(j->d_grads);
+    if (j->d_group_begin) (void)hipFree(j->d_group_begin);
+    if (j->d_segments) (void)hipFree(j->d_segments);
+    if (j->moments) (void)hipFree(j->moments);
+    if (j->weights) (void)hipFree(j->weights);
+    for (int i = 0; i < kStageSlots; ++i) {
+        if (j->stage_done[i]) (void)hipEventDestroy(j->stage_done[i]);
+        if (j->stage[i]) (void)hipHostFree(j->stage[i]);
+    }
+    if (j->own_stream && j->stream) (void)hipStreamDestroy(j->stream);
+    delete j;
+}
+
+int check_key(const phub_job* j, int key) {
+    if (key < 0 || key >= j->num_keys)
+        return fail(PHUB_EINVAL, "key %d out of range [0, %d)", key, j->num_keys);
+    return PHUB_OK;
+}
+
+int check_grad(const phub_job* j, int worker, int key, const float* grad) {
+    if (worker < 0 || worker >= j->num_workers)
+        return fail(PHUB_EINVAL, "worker %d out of range [0, %d)", worker, j->num_workers);
+    if (int rc = check_key(j, key)) return rc;
+    if (!grad && j->key_elems[key] != 0)
+        return fail(PHUB_EINVAL, "gradient of worker %d for key %d is NULL", worker, key);
+    if (reinterpret_cast<uintptr_t>(grad) % 16 != 0)
+        return fail(PHUB_EINVAL, "gradient of worker %d for key %d is not 16-byte aligned", worker,
+                    key);
+    return PHUB_OK;
+}
+
+void record_push(phub_job* j, int worker, int key, const float* grad) {
+    const size_t i = size_t(key) * j->num_workers + worker;
+    if (j->grads[i] != grad) {
+        j->grads[i] = grad;
+        j->table_dirty = true;
+    }
+    if (!j->pushed[i]) {
+        j->pushed[i] = 1;
+        ++j->num_pushed;
+    }
+}
+
+int upload_table(phub_job* j) {
+    const int slot = j->stage_next;
+    const size_t bytes = j->grads.size() * sizeof(const float*);
+    if (j->stage_used[slot]) {
+        hipError_t e = hipEventSynchronize(j->stage_done[slot]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize (pointer staging)");
+    }
+    std::memcpy(j->stage[slot], j->grads.data(), bytes);
+    hipError_t e = hipMemcpyAsync(j->d_grads, j->stage[slot], bytes, hipMemcpyHostToDevice,
+                                  j->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pointer table)");
+    e = hipEventRecord(j->stage_done[slot], j->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord (pointer staging)");
+    j->stage_used[slot] = true;
+    j->stage_next = (slot + 1) % kStageSlots;
+    j->table_dirty = false;
+    return PHUB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* phub_last_error(void) { return g_error.c_str(); }
+
+int phub_plan_count(int num_workers, int num_keys, const int64_t* key_elems, int64_t chunk_bytes,
+                    int num_groups, int min_items, int64_t* num_segments, int* groups_used,
+                    int64_t* item_elems) {
+    phub::Plan plan;
+    std::string err;
+    try {
+        err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, num_groups, min_items,
+                               &plan);
+    } catch (const std::bad_alloc&) {
+        return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
+    }
+    if (!err.empty()) return fail(PHUB_EINVAL, "%s", err.c_str());
+    if (num_segments) *num_segments = int64_t(plan.segments.size());
+    if (groups_used) *groups_used = plan.groups_used();
+    if (item_elems) *item_elems = plan.item_elems;
+    return PHUB_OK;
+}
+
+int phub_plan_build(int num_workers, int num_keys, const int64_t* key_elems, int64_t chunk_bytes,
+                    int num_groups, int min_items, phub_segment* segments, int64_t* group_begin,
+                    int64_t* group_cost) {
+    phub::Plan plan;
+    std::string err;
+    try {
+        err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, num_groups, min_items,
+                               &plan);
+    } catch (const std::bad_alloc&) {
+        return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
+    }
+    if (!err.empty()) return fail(PHUB_EINVAL, "%s", err.c_str());
+    if ((!segments && !plan.segments.empty()) || !group_begin)
+        return fail(PHUB_EINVAL, "output arrays are NULL");
+    for (size_t i = 0; i < plan.segments.size(); ++i)
+        segments[i] = {plan.segments[i].key, plan.segments[i].count, plan.segments[i].offset};
+    std::copy(plan.group_begin.begin(), plan.group_begin.end(), group_begin);
+    if (group_cost) std::copy(plan.group_cost.begin(), plan.group_cost.end(), group_cost);
+    return PHUB_OK;
+}
+
+int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_elems,
+              int64_t chunk_bytes, float lr, float momentum, float weight_decay, int nesterov,
+              void* hip_stream) {
+    if (!out) return fail(PHUB_EINVAL, "out is NULL");
+    *out = nullptr;
+    {
+        std::string err = phub::validate_shape(num_workers, num_keys, key_elems, chunk_bytes);
+        if (!err.empty()) return fail(PHUB_EINVAL, "%s", err.c_str());
+    }
+    if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
+        return fail(PHUB_EINVAL, "lr, momentum and weight_decay must be finite");
+
+    phub_job* j = new (std::nothrow) phub_job;
+    if (!j) return fail(PHUB_ENOMEM, "host allocation of the job failed");
+    int rc = PHUB_OK;
+    try {
+        j->num_workers = num_workers;
+        j->num_keys = num_keys;
+        j->key_elems.assign(key_elems, key_elems + num_keys);
+        j->arena_offset.resize(num_keys);
+        for (int k = 0; k < num_keys; ++k) {
+            j->arena_offset[k] = j->arena_elems;
+            j->arena_elems += (key_elems[k] + kArenaAlign - 1) / kArenaAlign * kArenaAlign;
+        }
+        j->chunk_bytes = chunk_bytes;
+        j->lr = lr;
+        j->mu = momentum;
+        j->wd = weight_decay;
+        j->nesterov = nesterov != 0;
+        j->grads.assign(size_t(num_workers) * num_keys, nullptr);
+        j->pushed.assign(size_t(num_workers) * num_keys, 0);
+    } catch (const std::bad_alloc&) {
+        delete j;
+        return fail(PHUB_ENOMEM, "host allocation of the job tables failed");
+    }
+
+    hipError_t e = hipGetDevice(&j->device);
+    if (e != hipSuccess) {
+        delete j;
+        return hip_fail(e, "hipGetDevice");
+    }
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, j->device);
+    if (e != hipSuccess || cus < 1) {
+        delete j;
+        return e != hipSuccess ? hip_fail(e, "hipDeviceGetAttribute(CU count)")
+                               : fail(PHUB_EHIP, "device reports no compute units");
+    }
+
+    phub::Plan plan;
+    {
+        const int64_t cap = PHUB_GROUPS_PER_CU > 0 ? int64_t(cus) * PHUB_GROUPS_PER_CU : (1 << 30);
+        std::string err;
+        try {
+            err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, int(cap), 2 * cus,
+                                   &plan);
+        } catch (const std::bad_alloc&) {
+            delete j;
+            return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
+        }
+        if (!err.empty()) {
+            delete j;
+            return fail(PHUB_EINVAL, "%s", err.c_str());
+        }
+    }
+    j->groups = plan.groups_used();
+    j->num_segments = int64_t(plan.segments.size());
+
+#define PHUB_TRY(call, what)                 \
+    do {                                     \
+        hipError_t e_ = (call);              \
+        if (e_ != hipSuccess) {              \
+            rc = hip_fail(e_, what);         \
+            goto fail_cleanup;               \
+        }                                    \
+    } while (0)
+
+    {
+        if (hip_stream) {
+            j->stream = static_cast<hipStream_t>(hip_stream);
+        } else {
+            PHUB_TRY(hipStreamCreateWithFlags(&j->stream, hipStreamNonBlocking), "hipStreamCreate");
+            j->own_stream = true;
+        }
+        const size_t arena_bytes = size_t(std::max<int64_t>(j->arena_elems, 1)) * sizeof(float);
+        if (hipMalloc(&j->weights, arena_bytes) != hipSuccess ||
+            hipMalloc(&j->moments, arena_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            rc = fail(PHUB_ENOMEM, "device allocation of W and M (%zu bytes each) failed",
+                      arena_bytes);
+            goto fail_cleanup;
+        }
+        PHUB_TRY(hipMemsetAsync(j->weights, 0, arena_bytes, j->stream), "hipMemsetAsync(W)");
+        PHUB_TRY(hipMemsetAsync(j->moments, 0, arena_bytes, j->stream), "hipMemsetAsync(M)");
+
+        std::vector<phub::DevSegment> dseg(plan.segments.size());
+        for (size_t i = 0; i < plan.segments.size(); ++i) {
+            const phub::PlanSegment& s = plan.segments[i];
+            dseg[i] = {j->arena_offset[s.key] + s.offset, s.offset, s.key, s.count, 0};
+        }
+        const size_t seg_bytes = std::max<size_t>(dseg.size(), 1) * sizeof(phub::DevSegment);
+        const size_t gb_bytes = plan.group_begin.size() * sizeof(int64_t);
+        const size_t tab_bytes = j->grads.size() * sizeof(const float*);
+        if (hipMalloc(&j->d_segments, seg_bytes) != hipSuccess ||
+            hipMalloc(&j->d_group_begin, gb_bytes) != hipSuccess ||
+            hipMalloc(&j->d_grads, tab_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            rc = fail(PHUB_ENOMEM, "device allocation of the schedule failed");
+            goto fail_cleanup;
+        }
+        if (!dseg.empty())
+            PHUB_TRY(hipMemcpy(j->d_segments, dseg.data(), dseg.size() * sizeof(phub::DevSegment),
+                               hipMemcpyHostToDevice),
+                     "hipMemcpy(schedule)");
+        PHUB_TRY(hipMemcpy(j->d_group_begin, plan.group_begin.data(), gb_bytes,
+                           hipMemcpyHostToDevice),
+                 "hipMemcpy(group table)");
+        for (int i = 0; i < kStageSlots; ++i) {
+            if (hipHostMalloc(reinterpret_cast<void**>(&j->stage[i]), tab_bytes,
+                              hipHostMallocDefault) != hipSuccess) {
+                (void)hipGetLastError();
+                rc = fail(PHUB_ENOMEM, "pinned host allocation of the pointer staging failed");
+                goto fail_cleanup;
+            }
+            PHUB_TRY(hipEventCreateWithFlags(&j->stage_done[i], hipEventDisableTiming),
+                     "hipEventCreate");
+        }
+        PHUB_TRY(hipStreamSynchronize(j->stream), "hipStreamSynchronize (init)");
+    }
+#undef PHUB_TRY
+
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        g_live.insert(j);
+    }
+    *out = j;
+    return PHUB_OK;
+
+fail_cleanup:
+    release(j);
+    return rc;
+}
+
+int phub_set_weights(phub_job* j, int key, const float* src) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (int rc = check_key(j, key)) return rc;
+    const int64_t n = j->key_elems[key];
+    if (n == 0) return PHUB_OK;
+    if (!src) return fail(PHUB_EINVAL, "src is NULL");
+    DeviceScope ds(j->device);
+    if (!ds.ok()) return fail(PHUB_EHIP, "cannot make device %d current", j->device);
+    const size_t bytes = size_t(n) * sizeof(float);
+    hipError_t e = hipMemcpyAsync(j->weights + j->arena_offset[key], src, bytes, hipMemcpyDefault,
+                                  j->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(set_weights)");
+    e = hipMemsetAsync(j->moments + j->arena_offset[key], 0, bytes, j->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(momentum)");
+    return PHUB_OK;
+}
+
+int phub_push(phub_job* j, int worker, int key, const float* grad) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (int rc = check_grad(j, worker, key, grad)) return rc;
+    record_push(j, worker, key, grad);
+    return PHUB_OK;
+}
+
+int phub_push_keys(phub_job* j, int worker, int count, const int* keys,
+                   const float* const* grads) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (count < 0) return fail(PHUB_EINVAL, "count %d is negative", count);
+    if (count > 0 && !grads) return fail(PHUB_EINVAL, "grads is NULL");
+    if (!keys && count > j->num_keys)
+        return fail(PHUB_EINVAL, "count %d exceeds the %d keys", count, j->num_keys);
+    for (int i = 0; i < count; ++i)
+        if (int rc = check_grad(j, worker, keys ? keys[i] : i, grads[i])) return rc;
+    for (int i = 0; i < count; ++i) record_push(j, worker, keys ? keys[i] : i, grads[i]);
+    return PHUB_OK;
+}
+
+int phub_step(phub_job* j) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    const int64_t need = int64_t(j->num_workers) * j->num_keys;
+    if (j->num_pushed != need) {
+        for (size_t i = 0; i < j->pushed.size(); ++i)
+            if (!j->pushed[i])
+                return fail(PHUB_ENOTREADY,
+                            "%lld of %lld (worker, key) pairs pushed; worker %d has not pushed key %d",
+                            (long long)j->num_pushed, (long long)need, int(i % j->num_workers),
+                            int(i / j->num_workers));
+    }
+    DeviceScope ds(j->device);
+    if (!ds.ok()) return fail(PHUB_EHIP, "cannot make device %d current", j->device);
+    if (j->table_dirty)
+        if (int rc = upload_table(j)) return rc;
+    if (j->groups > 0) {
+        phub::StepParams p;
+        p.segments = j->d_segments;
+        p.group_begin = j->d_group_begin;
+        p.grads = j->d_grads;
+        p.weights = j->weights;
+        p.moments = j->moments;
+        p.lr = j->lr;
+        p.mu = j->mu;
+        p.wd = j->wd;
+        p.num_workers = j->num_workers;
+        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->groups, j->block, j->stream);
+        if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
+    }
+    std::fill(j->pushed.begin(), j->pushed.end(), 0);
+    j->num_pushed = 0;
+    return PHUB_OK;
+}
+
+int phub_pull(phub_job* j, int key, const float** weights) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (int rc = check_key(j, key)) return rc;
+    if (!weights) return fail(PHUB_EINVAL, "weights is NULL");
+    *weights = j->weights + j->arena_offset[key];
+    return PHUB_OK;
+}
+
+int phub_get_state(phub_job* j, int key, const float** weights, const float** momentum) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (int rc = check_key(j, key)) return rc;
+    if (weights) *weights = j->weights + j->arena_offset[key];
+    if (momentum) *momentum = j->moments + j->arena_offset[key];
+    return PHUB_OK;
+}
+
+int phub_sync(phub_job* j) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    DeviceScope ds(j->device);
+    if (!ds.ok()) return fail(PHUB_EHIP, "cannot make device %d current", j->device);
+    hipError_t e = hipStreamSynchronize(j->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    return PHUB_OK;
+}
+
+int phub_get_stream(phub_job* j, void** hip_stream) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (!hip_stream) return fail(PHUB_EINVAL, "hip_stream is NULL");
+    *hip_stream = j->stream;
+    return PHUB_OK;
+}
+
+int phub_job_info(phub_job* j, int* workgroups, int* threads_per_group, int64_t* segments) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (workgroups) *workgroups = j->groups;
+    if (threads_per_group) *threads_per_group = j->block;
+    if (segments) *segments = j->num_segments;
+    return PHUB_OK;
+}
+
+int phub_destroy(phub_job* j) {
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        if (!j || g_live.erase(j) == 0) return fail(PHUB_ESTATE, "not a live job handle");
+    }
+    DeviceScope ds(j->device);
+    hipError_t e = hipStreamSynchronize(j->stream);
+    release(j);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize (destroy)");
+    return PHUB_OK;
+}
+
+}  // extern "C"

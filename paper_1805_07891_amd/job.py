@@ -1,0 +1,139 @@
+"""One exchange job over torch-allocated device memory.
+
+Plumbing only: torch allocates the worker gradient arenas and the stream,
+this class turns them into the pointers the C interface takes, and copies
+the job's state out for inspection.  All arithmetic of the step runs in the
+HIP library.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+from . import phub as _phub
+from .workloads import Job, key_offsets
+
+HIP_MEMCPY_DEFAULT = 4
+
+_hip = None
+
+
+def hip_runtime():
+    """The HIP runtime torch loaded (same SONAME as the library links)."""
+    global _hip
+    if _hip is None:
+        import torch  # noqa: F401  (loads torch's libamdhip64.so.7 first)
+        lib = ctypes.CDLL("libamdhip64.so.7")
+        lib.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        lib.hipMemcpy.restype = ctypes.c_int
+        _hip = lib
+    return _hip
+
+
+def copy_to_host(dst: np.ndarray, src_ptr: int) -> None:
+    """Synchronous copy of dst.nbytes from device address src_ptr."""
+    rc = hip_runtime().hipMemcpy(dst.ctypes.data, src_ptr, dst.nbytes, HIP_MEMCPY_DEFAULT)
+    if rc != 0:
+        raise RuntimeError(f"hipMemcpy to host failed with code {rc}")
+
+
+def load_library(path: Optional[str] = None) -> _phub.Library:
+    import torch  # noqa: F401  (one HIP runtime for torch and the library)
+    return _phub.load(path)
+
+
+class TorchJob:
+    """A phub job plus the torch buffers of its N workers.
+
+    Gradients of worker w live in one arena tensor of ``arena_elems`` fp32
+    values, key k at element offset ``offsets[k]`` (256-byte aligned); the
+    job's own W and M arenas use the same layout.
+    """
+
+    def __init__(self, spec: Job, device, stream=None, chunk_bytes: Optional[int] = None,
+                 lib: Optional[_phub.Library] = None):
+        import torch
+        self.torch = torch
+        self.spec = spec
+        self.device = torch.device(device)
+        self.lib = lib or load_library()
+        self.stream = stream if stream is not None else torch.cuda.Stream(device=self.device)
+        self.offsets, self.arena_elems = key_offsets(spec.key_elems)
+        self.chunk_bytes = spec.chunk_bytes if chunk_bytes is None else int(chunk_bytes)
+        with torch.cuda.device(self.device):
+            self.handle = self.lib.phub_init(spec.num_workers, spec.key_elems, self.chunk_bytes,
+                                             spec.lr, spec.momentum, spec.weight_decay,
+                                             spec.nesterov, self.stream.cuda_stream)
+        self._ptr_arrays: List = [None] * spec.num_workers
+        self._grad_refs: List = [None] * spec.num_workers
+
+    # -- inputs ----------------------------------------------------------------
+    def key_pointers(self, arena) -> List[int]:
+        base = arena.data_ptr()
+        return [base + 4 * off for off in self.offsets]
+
+    def attach_grads(self, worker: int, arena) -> None:
+        """Use ``arena`` (a device fp32 tensor of arena_elems values) as
+        worker ``worker``'s gradients from now on."""
+        if arena.numel() != self.arena_elems or arena.dtype != self.torch.float32:
+            raise ValueError("gradient arena has the wrong size or dtype")
+        self._grad_refs[worker] = arena
+        self._ptr_arrays[worker] = _phub.pointer_array(self.key_pointers(arena))
+
+    def set_weights(self, arena) -> None:
+        """Load every key's weights from a device arena (and zero M).  The
+        job's stream first waits for work already queued on torch's current
+        stream (which typically produced ``arena``)."""
+        self.stream.wait_stream(self.torch.cuda.current_stream(self.device))
+        self._weights_src = arena
+        ptrs = self.key_pointers(arena)
+        for k in range(self.spec.num_keys):
+            self.lib.phub_set_weights(self.handle, k, ptrs[k])
+
+    # -- the step --------------------------------------------------------------
+    def push_all(self) -> None:
+        for w, arr in enumerate(self._ptr_arrays):
+            if arr is None:
+                raise RuntimeError(f"worker {w} has no gradient arena attached")
+            self.lib.phub_push_keys(self.handle, w, arr)
+
+    def step(self) -> None:
+        self.lib.phub_step(self.handle)
+
+    def push_and_step(self) -> None:
+        self.push_all()
+        self.step()
+
+    def sync(self) -> None:
+        self.lib.phub_sync(self.handle)
+
+    # -- outputs ---------------------------------------------------------------
+    def state_arenas(self):
+        """(W, M) copied to host as numpy arenas of arena_elems values."""
+        self.sync()
+        w_ptr, m_ptr = self.lib.phub_get_state(self.handle, 0)
+        W = np.empty(self.arena_elems, dtype=np.float32)
+        M = np.empty(self.arena_elems, dtype=np.float32)
+        copy_to_host(W, w_ptr)
+        copy_to_host(M, m_ptr)
+        return W, M
+
+    def split(self, arena: np.ndarray) -> List[np.ndarray]:
+        return [arena[o:o + n] for o, n in zip(self.offsets, self.spec.key_elems)]
+
+    def info(self):
+        return self.lib.phub_job_info(self.handle)
+
+    def destroy(self) -> None:
+        if self.handle is not None:
+            self.lib.phub_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass

@@ -1,0 +1,194 @@
+"""Python binding of the C interface in ``include/phub.h`` (ctypes).
+
+Argument marshalling only: every step of the exchange runs in the HIP
+library ``libphub.so``.  The functions keep the C names; each returns the C
+status code, raising ``PhubError`` for a nonzero one unless ``check=False``.
+Pointers are plain integers (torch's ``tensor.data_ptr()``, a stream's
+``cuda_stream``).  If the library is not built, loading raises ImportError:
+there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+DEFAULT_LIB = os.path.join(PKG, "libphub.so")
+
+PHUB_OK = 0
+PHUB_EINVAL = -1
+PHUB_ENOTREADY = -2
+PHUB_ENOMEM = -3
+PHUB_EHIP = -4
+PHUB_ESTATE = -5
+
+STATUS_NAMES = {0: "PHUB_OK", -1: "PHUB_EINVAL", -2: "PHUB_ENOTREADY", -3: "PHUB_ENOMEM",
+                -4: "PHUB_EHIP", -5: "PHUB_ESTATE"}
+
+# Every symbol the header declares.
+EXPORTED = ("phub_init", "phub_set_weights", "phub_push", "phub_push_keys", "phub_step",
+            "phub_pull", "phub_get_state", "phub_sync", "phub_get_stream", "phub_job_info",
+            "phub_destroy", "phub_last_error", "phub_plan_count", "phub_plan_build")
+
+
+class PhubError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {message}")
+        self.code = code
+
+
+class PhubSegment(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_int32), ("count", ctypes.c_int32), ("offset", ctypes.c_int64)]
+
+
+class Library:
+    """The C functions of one built ``libphub.so``."""
+
+    def __init__(self, path: str = DEFAULT_LIB):
+        if not os.path.exists(path):
+            raise ImportError(f"HIP library {path} is not built; run __graft_entry__.build()")
+        self.path = path
+        lib = ctypes.CDLL(path)
+        vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
+        pp = ctypes.POINTER(ctypes.c_void_p)
+        sig = {
+            "phub_init": ([pp, i32, i32, vp, i64, f32, f32, f32, i32, vp], i32),
+            "phub_set_weights": ([vp, i32, vp], i32),
+            "phub_push": ([vp, i32, i32, vp], i32),
+            "phub_push_keys": ([vp, i32, i32, vp, vp], i32),
+            "phub_step": ([vp], i32),
+            "phub_pull": ([vp, i32, pp], i32),
+            "phub_get_state": ([vp, i32, pp, pp], i32),
+            "phub_sync": ([vp], i32),
+            "phub_get_stream": ([vp, pp], i32),
+            "phub_job_info": ([vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64)], i32),
+            "phub_destroy": ([vp], i32),
+            "phub_last_error": ([], ctypes.c_char_p),
+            "phub_plan_count": ([i32, i32, vp, i64, i32, i32, ctypes.POINTER(i64),
+                                 ctypes.POINTER(i32), ctypes.POINTER(i64)], i32),
+            "phub_plan_build": ([i32, i32, vp, i64, i32, i32, vp, vp, vp], i32),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        self.lib = lib
+
+    def _check(self, rc: int, check: bool) -> int:
+        if rc != 0 and check:
+            raise PhubError(rc, self.last_error())
+        return rc
+
+    def last_error(self) -> str:
+        return self.lib.phub_last_error().decode()
+
+    # -- job lifecycle -----------------------------------------------------
+    def phub_init(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
+                  lr: float, momentum: float, weight_decay: float, nesterov: bool,
+                  hip_stream: Optional[int] = None, check: bool = True):
+        """Returns the job handle (an int), or (rc, None) with check=False on error."""
+        elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
+        out = ctypes.c_void_p()
+        rc = self.lib.phub_init(ctypes.byref(out), int(num_workers), len(key_elems),
+                                ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes),
+                                float(lr), float(momentum), float(weight_decay),
+                                int(bool(nesterov)), hip_stream)
+        if rc != 0:
+            self._check(rc, check)
+            return rc, None
+        return out.value
+
+    def phub_set_weights(self, job, key: int, src_ptr: int, check: bool = True) -> int:
+        return self._check(self.lib.phub_set_weights(job, int(key), src_ptr), check)
+
+    def phub_push(self, job, worker: int, key: int, grad_ptr: int, check: bool = True) -> int:
+        return self._check(self.lib.phub_push(job, int(worker), int(key), grad_ptr), check)
+
+    def phub_push_keys(self, job, worker: int, grad_ptrs, keys=None, check: bool = True) -> int:
+        """grad_ptrs: a ctypes c_void_p array (see ``pointer_array``) or a
+        sequence of ints; keys: None (0..count-1) or a sequence of ints."""
+        if not isinstance(grad_ptrs, ctypes.Array):
+            grad_ptrs = pointer_array(grad_ptrs)
+        karr = None
+        if keys is not None:
+            karr = (ctypes.c_int * len(keys))(*[int(k) for k in keys])
+        return self._check(self.lib.phub_push_keys(job, int(worker), len(grad_ptrs),
+                                                   karr, grad_ptrs), check)
+
+    def phub_step(self, job, check: bool = True) -> int:
+        return self._check(self.lib.phub_step(job), check)
+
+    def phub_pull(self, job, key: int) -> int:
+        out = ctypes.c_void_p()
+        self._check(self.lib.phub_pull(job, int(key), ctypes.byref(out)), True)
+        return out.value or 0
+
+    def phub_get_state(self, job, key: int):
+        w, m = ctypes.c_void_p(), ctypes.c_void_p()
+        self._check(self.lib.phub_get_state(job, int(key), ctypes.byref(w), ctypes.byref(m)), True)
+        return (w.value or 0), (m.value or 0)
+
+    def phub_sync(self, job, check: bool = True) -> int:
+        return self._check(self.lib.phub_sync(job), check)
+
+    def phub_get_stream(self, job) -> int:
+        out = ctypes.c_void_p()
+        self._check(self.lib.phub_get_stream(job, ctypes.byref(out)), True)
+        return out.value or 0
+
+    def phub_job_info(self, job):
+        g, t, s = ctypes.c_int(), ctypes.c_int(), ctypes.c_int64()
+        self._check(self.lib.phub_job_info(job, ctypes.byref(g), ctypes.byref(t), ctypes.byref(s)), True)
+        return g.value, t.value, s.value
+
+    def phub_destroy(self, job, check: bool = True) -> int:
+        return self._check(self.lib.phub_destroy(job), check)
+
+    # -- schedule (host only) ----------------------------------------------
+    def phub_plan_count(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
+                        num_groups: int, min_items: int = 0):
+        elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
+        nseg, used, item = ctypes.c_int64(), ctypes.c_int(), ctypes.c_int64()
+        self._check(self.lib.phub_plan_count(int(num_workers), len(key_elems),
+                                             ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes),
+                                             int(num_groups), int(min_items), ctypes.byref(nseg),
+                                             ctypes.byref(used), ctypes.byref(item)), True)
+        return nseg.value, used.value, item.value
+
+    def phub_plan_build(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
+                        num_groups: int, min_items: int = 0):
+        """Returns (segments as a list of (key, count, offset), group_begin,
+        group_cost, item_elems)."""
+        nseg, used, item = self.phub_plan_count(num_workers, key_elems, chunk_bytes, num_groups,
+                                                min_items)
+        elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
+        segs = (PhubSegment * max(nseg, 1))()
+        gb = (ctypes.c_int64 * (used + 1))()
+        gc = (ctypes.c_int64 * max(used, 1))()
+        self._check(self.lib.phub_plan_build(int(num_workers), len(key_elems),
+                                             ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes),
+                                             int(num_groups), int(min_items), segs, gb, gc), True)
+        seg_list = [(segs[i].key, segs[i].count, segs[i].offset) for i in range(nseg)]
+        return seg_list, list(gb), list(gc[:used]), item
+
+
+def pointer_array(ptrs: Sequence[int]):
+    arr = (ctypes.c_void_p * len(ptrs))()
+    for i, p in enumerate(ptrs):
+        arr[i] = int(p)
+    return arr
+
+
+_default: Optional[Library] = None
+
+
+def load(path: Optional[str] = None) -> Library:
+    """The library at ``path`` (default: the in-tree build)."""
+    global _default
+    if path is not None and path != DEFAULT_LIB:
+        return Library(path)
+    if _default is None:
+        _default = Library(DEFAULT_LIB)
+    return _default

@@ -1,0 +1,378 @@
+"""GPU parity of the fused exchange step against the CPU oracle.
+
+Every test drives the HIP library through its C interface (ctypes binding)
+on seeded synthetic inputs and compares the job's master weights W and
+momentum M with the oracle's, element by element.  The accumulation order
+is pinned on both sides (ascending worker index) and both evaluate the same
+fused multiply-adds, so the bar is bit-exact equality; the 1e-6 relative
+tolerance is reported alongside as a diagnostic.
+"""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1805_07891_amd import phub, workloads
+from paper_1805_07891_amd.job import TorchJob, load_library
+from paper_1805_07891_amd.workloads import Job, key_offsets
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    return torch, torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def lib(torch_dev):
+    return load_library()
+
+
+def _bits_equal(a, b):
+    return np.array_equal(np.asarray(a, np.float32).view(np.uint32),
+                          np.asarray(b, np.float32).view(np.uint32))
+
+
+def _rel_err(x, ref):
+    ref = ref.astype(np.float64)
+    if ref.size == 0:
+        return 0.0
+    rms = np.sqrt(np.mean(ref ** 2)) or 1.0
+    return float(np.max(np.abs(x.astype(np.float64) - ref) / np.maximum(np.abs(ref), rms)))
+
+
+def run_small_case(torch, dev, lib, n_workers, key_elems, steps=2, chunk_bytes=32768,
+                   lr=0.1, mu=0.9, wd=1e-4, nesterov=True, seed=0, push="keys",
+                   reuse_buffers=False, stream=None):
+    """Runs `steps` steps on the GPU and in the oracle; returns the job and
+    per-step (gpu W, gpu M, oracle W, oracle M) lists per key."""
+    spec = Job("case", n_workers, tuple(int(n) for n in key_elems), chunk_elems=chunk_bytes // 4,
+               lr=lr, momentum=mu, weight_decay=wd, nesterov=nesterov, sigma_g=1e-2)
+    job = TorchJob(spec, dev, stream=stream, chunk_bytes=chunk_bytes, lib=lib)
+    offs, total = key_offsets(spec.key_elems)
+    rng = np.random.default_rng(seed)
+    w0 = np.zeros(total, np.float32)
+    for o, n in zip(offs, spec.key_elems):
+        w0[o:o + n] = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
+    job.set_weights(torch.from_numpy(w0).to(dev))
+    W = [w0[o:o + n].copy() for o, n in zip(offs, spec.key_elems)]
+    M = [np.zeros(n, np.float32) for n in spec.key_elems]
+    dev_arenas = None
+    results = []
+    for t in range(steps):
+        host = []
+        for w in range(n_workers):
+            a = np.zeros(total, np.float32)
+            for o, n in zip(offs, spec.key_elems):
+                a[o:o + n] = rng.standard_normal(n, dtype=np.float32) * np.float32(1e-2)
+            host.append(a)
+        if reuse_buffers and dev_arenas is not None:
+            for w in range(n_workers):
+                dev_arenas[w].copy_(torch.from_numpy(host[w]))
+        else:
+            dev_arenas = [torch.from_numpy(a).to(dev) for a in host]
+            for w in range(n_workers):
+                job.attach_grads(w, dev_arenas[w])
+        torch.cuda.synchronize()
+        if push == "keys":
+            job.push_all()
+        elif push == "single_reversed":
+            for k in reversed(range(spec.num_keys)):
+                for w in reversed(range(n_workers)):
+                    lib.phub_push(job.handle, w, k, job.key_pointers(dev_arenas[w])[k])
+        else:
+            raise ValueError(push)
+        job.step()
+        oracle.step([[h[o:o + n] for o, n in zip(offs, spec.key_elems)] for h in host],
+                    W, M, lr, mu, wd, nesterov)
+        Wg, Mg = job.state_arenas()
+        results.append((job.split(Wg), job.split(Mg), [x.copy() for x in W], [x.copy() for x in M]))
+    return job, results
+
+
+def assert_parity(results, label=""):
+    for t, (wg, mg, wo, mo) in enumerate(results):
+        for k in range(len(wo)):
+            if not _bits_equal(wg[k], wo[k]) or not _bits_equal(mg[k], mo[k]):
+                raise AssertionError(
+                    f"{label} step {t} key {k} (n={wo[k].size}): W rel err {_rel_err(wg[k], wo[k]):.3g}, "
+                    f"M rel err {_rel_err(mg[k], mo[k]):.3g}; first W mismatch at "
+                    f"{int(np.argmax(wg[k].view(np.uint32) != wo[k].view(np.uint32)))}")
+
+
+def test_library_is_in_tree_and_shares_torchs_hip_runtime(lib, torch_dev):
+    torch, dev = torch_dev
+    torch.zeros(1, device=dev)
+    with open("/proc/self/maps") as f:
+        maps = f.read()
+    hip = {line.split()[-1] for line in maps.splitlines() if "libamdhip64" in line}
+    assert len(hip) == 1, f"more than one HIP runtime mapped: {hip}"
+    phubs = {line.split()[-1] for line in maps.splitlines() if line.endswith("libphub.so")}
+    assert phubs == {os.path.realpath(phub.DEFAULT_LIB)}, phubs
+
+
+def test_tiny_workload_full_parity(lib, torch_dev):
+    torch, dev = torch_dev
+    wl = workloads.workload("tiny")
+    spec = wl.jobs[0]
+    _say("tiny: N", spec.num_workers, "K", spec.num_keys, "P", spec.num_params)
+    job, res = run_small_case(torch, dev, lib, spec.num_workers, spec.key_elems, steps=wl.steps,
+                              chunk_bytes=spec.chunk_bytes, lr=spec.lr, mu=spec.momentum,
+                              wd=spec.weight_decay, nesterov=spec.nesterov, seed=1805)
+    assert_parity(res, "tiny")
+    job.destroy()
+
+
+EDGE = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 63, 64, 65, 1023, 1024, 1025, 8191, 8192, 8193,
+        2 * 8192 + 3, 0, 3 * 8192]
+
+
+@pytest.mark.parametrize("n_workers", [1, 2, 3, 5, 8, 11, 16, 17, 33])
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_edge_shapes(lib, torch_dev, n_workers, nesterov):
+    torch, dev = torch_dev
+    _say("edge shapes N", n_workers, "nesterov", nesterov)
+    job, res = run_small_case(torch, dev, lib, n_workers, EDGE, steps=2, nesterov=nesterov,
+                              seed=100 + n_workers)
+    assert_parity(res, f"N={n_workers}")
+    job.destroy()
+
+
+@pytest.mark.parametrize("hp", [dict(mu=0.0), dict(lr=0.0), dict(wd=0.0, mu=0.0),
+                                dict(lr=0.5, mu=0.5, wd=0.25), dict(lr=-1.0, mu=0.99, wd=0.3)])
+def test_hyperparameter_corners(lib, torch_dev, hp):
+    torch, dev = torch_dev
+    for nest in (True, False):
+        job, res = run_small_case(torch, dev, lib, 4, [5, 8192, 10007], steps=2, nesterov=nest,
+                                  seed=7, **hp)
+        assert_parity(res, f"{hp} nesterov={nest}")
+        job.destroy()
+
+
+def test_chunk_size_does_not_change_results(lib, torch_dev):
+    torch, dev = torch_dev
+    keys = [3, 100, 8192 * 3 + 5, 70000, 1]
+    outs = []
+    for cb in (16, 48, 4096, 32768, 1 << 22):
+        _say("chunk bytes", cb)
+        job, res = run_small_case(torch, dev, lib, 6, keys, steps=2, chunk_bytes=cb, seed=99)
+        assert_parity(res, f"chunk={cb}")
+        outs.append(res[-1][:2])
+        job.destroy()
+    for wg, mg in outs[1:]:
+        for k in range(len(keys)):
+            assert _bits_equal(wg[k], outs[0][0][k]) and _bits_equal(mg[k], outs[0][1][k])
+
+
+def test_push_order_and_single_pushes(lib, torch_dev):
+    torch, dev = torch_dev
+    keys = [17, 9000, 4]
+    job, res = run_small_case(torch, dev, lib, 5, keys, steps=2, seed=5, push="single_reversed")
+    assert_parity(res, "reversed single pushes")
+    job.destroy()
+
+
+def test_reused_buffers_skip_pointer_upload(lib, torch_dev):
+    torch, dev = torch_dev
+    job, res = run_small_case(torch, dev, lib, 4, [1000, 20000], steps=3, seed=6,
+                              reuse_buffers=True)
+    assert_parity(res, "reused buffers")
+    job.destroy()
+
+
+def test_step_before_all_pushes_is_refused(lib, torch_dev):
+    torch, dev = torch_dev
+    spec = Job("nr", 3, (100, 200))
+    job = TorchJob(spec, dev, lib=lib)
+    arenas = [torch.randn(job.arena_elems, device=dev) for _ in range(3)]
+    for w in range(3):
+        job.attach_grads(w, arenas[w])
+    W0, M0 = job.state_arenas()
+    for w in range(2):
+        lib.phub_push_keys(job.handle, w, job._ptr_arrays[w])
+    lib.phub_push(job.handle, 2, 0, job.key_pointers(arenas[2])[0])
+    assert lib.phub_step(job.handle, check=False) == phub.PHUB_ENOTREADY
+    assert "worker 2" in lib.last_error() and "key 1" in lib.last_error()
+    W1, M1 = job.state_arenas()
+    assert _bits_equal(W0, W1) and _bits_equal(M0, M1)
+    # completing the pushes makes the step go
+    lib.phub_push(job.handle, 2, 1, job.key_pointers(arenas[2])[1])
+    lib.phub_step(job.handle)
+    job.sync()
+    # after a step every pair counts as not pushed again
+    assert lib.phub_step(job.handle, check=False) == phub.PHUB_ENOTREADY
+    job.destroy()
+
+
+def test_argument_errors_on_a_live_job(lib, torch_dev):
+    torch, dev = torch_dev
+    spec = Job("err", 2, (100, 0))
+    job = TorchJob(spec, dev, lib=lib)
+    buf = torch.zeros(1024, device=dev)
+    p = buf.data_ptr()
+    assert lib.phub_push(job.handle, 0, 0, p + 4, check=False) == phub.PHUB_EINVAL  # misaligned
+    assert lib.phub_push(job.handle, 2, 0, p, check=False) == phub.PHUB_EINVAL      # worker
+    assert lib.phub_push(job.handle, 0, 2, p, check=False) == phub.PHUB_EINVAL      # key
+    assert lib.phub_push(job.handle, 0, 0, 0, check=False) == phub.PHUB_EINVAL      # null
+    assert lib.phub_push(job.handle, 0, 1, 0, check=False) == phub.PHUB_OK          # empty key
+    assert lib.phub_push_keys(job.handle, 1, [p, p + 4], check=False) == phub.PHUB_EINVAL
+    assert lib.phub_push_keys(job.handle, 1, [p, p, p], check=False) == phub.PHUB_EINVAL
+    h = job.handle
+    job.destroy()
+    assert lib.phub_step(h, check=False) == phub.PHUB_ESTATE
+    assert lib.phub_destroy(h, check=False) == phub.PHUB_ESTATE
+
+
+def test_all_keys_empty(lib, torch_dev):
+    torch, dev = torch_dev
+    spec = Job("empty", 2, (0, 0, 0))
+    job = TorchJob(spec, dev, lib=lib)
+    for w in range(2):
+        for k in range(3):
+            lib.phub_push(job.handle, w, k, 0)
+    lib.phub_step(job.handle)
+    job.sync()
+    assert job.info()[0] == 0
+    job.destroy()
+
+
+def test_set_weights_resets_momentum(lib, torch_dev):
+    torch, dev = torch_dev
+    job, res = run_small_case(torch, dev, lib, 2, [300], steps=2, seed=8)
+    new_w = torch.full((job.arena_elems,), 0.5, device=dev)
+    job.set_weights(new_w)
+    W, M = job.state_arenas()
+    assert np.all(W[:300] == 0.5) and np.all(M[:300] == 0.0)
+    job.destroy()
+
+
+def test_concurrent_jobs_equal_sequential(lib, torch_dev):
+    torch, dev = torch_dev
+    specs = [(8, [70000, 3, 8193]), (4, [12345, 64]), (16, [30000]), (3, [1, 2, 3, 100000])]
+    # concurrent: one stream each, steps interleaved
+    seq = [run_small_case(torch, dev, lib, n, k, steps=2, seed=40 + i) for i, (n, k) in enumerate(specs)]
+    for job, res in seq:
+        assert_parity(res, "sequential")
+        job.destroy()
+    streams = [torch.cuda.Stream(device=dev) for _ in specs]
+    jobs = []
+    rng_inputs = []
+    for i, (n, keys) in enumerate(specs):
+        spec = Job(f"c{i}", n, tuple(keys))
+        job = TorchJob(spec, dev, stream=streams[i], lib=lib)
+        offs, total = key_offsets(keys)
+        rng = np.random.default_rng(40 + i)
+        w0 = np.zeros(total, np.float32)
+        for o, m in zip(offs, keys):
+            w0[o:o + m] = rng.standard_normal(m, dtype=np.float32) * np.float32(0.05)
+        job.set_weights(torch.from_numpy(w0).to(dev))
+        steps_host = []
+        for t in range(2):
+            host = []
+            for w in range(n):
+                a = np.zeros(total, np.float32)
+                for o, m in zip(offs, keys):
+                    a[o:o + m] = rng.standard_normal(m, dtype=np.float32) * np.float32(1e-2)
+                host.append(a)
+            steps_host.append([torch.from_numpy(a).to(dev) for a in host])
+        jobs.append(job)
+        rng_inputs.append(steps_host)
+    torch.cuda.synchronize()
+    for t in range(2):
+        for job, inputs in zip(jobs, rng_inputs):
+            for w, a in enumerate(inputs[t]):
+                job.attach_grads(w, a)
+            job.push_and_step()
+    for i, job in enumerate(jobs):
+        W, M = job.state_arenas()
+        wg, mg = job.split(W), job.split(M)
+        sw, sm = seq[i][1][-1][0], seq[i][1][-1][1]
+        for k in range(len(wg)):
+            assert _bits_equal(wg[k], sw[k]) and _bits_equal(mg[k], sm[k]), (i, k)
+        job.destroy()
+
+
+# --------------------------------------------------------------------------
+# Full-size workloads in the benchmark's launch configuration, checked on
+# sampled elements that the oracle recomputes one by one.
+# --------------------------------------------------------------------------
+
+def _sample_positions(spec, rng, n_random=20000):
+    """Element positions (key, index) covering random elements, each key's
+    first and last elements and elements around chunk boundaries."""
+    pos = set()
+    C = spec.chunk_elems
+    for k, n in enumerate(spec.key_elems):
+        for i in list(range(min(n, 3))) + list(range(max(0, n - 5), n)):
+            pos.add((k, i))
+        if n > C:
+            for c in range(C, n, C)[:4]:
+                for i in (c - 1, c, c + 1):
+                    if i < n:
+                        pos.add((k, i))
+    P = spec.num_params
+    flat = rng.integers(0, P, size=n_random)
+    bounds = np.cumsum([0] + list(spec.key_elems))
+    keys = np.searchsorted(bounds, flat, side="right") - 1
+    for k, f in zip(keys, flat):
+        pos.add((int(k), int(f - bounds[k])))
+    return sorted(pos)
+
+
+@pytest.mark.parametrize("name", ["resnet50", "alexnet", "resnet269", "multitenant"])
+def test_full_size_workload_sampled(lib, torch_dev, name):
+    torch, dev = torch_dev
+    wl = workloads.workload(name)
+    steps = 2
+    _say("full size", name, workloads.describe(wl))
+    jobs, grads, w0s = [], [], []
+    for ji, spec in enumerate(wl.jobs):
+        stream = torch.cuda.Stream(device=dev)
+        job = TorchJob(spec, dev, stream=stream, lib=lib)
+        w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
+        job.set_weights(w0)
+        g = [[workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, t, w)
+              for w in range(spec.num_workers)] for t in range(steps)]
+        jobs.append(job)
+        grads.append(g)
+        w0s.append(w0)
+    torch.cuda.synchronize()
+    for t in range(steps):
+        for job, g in zip(jobs, grads):
+            for w, a in enumerate(g[t]):
+                job.attach_grads(w, a)
+            job.push_and_step()
+    for ji, (job, spec) in enumerate(zip(jobs, wl.jobs)):
+        W, M = job.state_arenas()
+        rng = np.random.default_rng(ji)
+        pos = _sample_positions(spec, rng)
+        idx = np.array([job.offsets[k] + i for k, i in pos], dtype=np.int64)
+        tidx = torch.from_numpy(idx).to(dev)
+        gs = [[grads[ji][t][w].index_select(0, tidx).cpu().numpy() for w in range(spec.num_workers)]
+              for t in range(steps)]
+        ws = w0s[ji].index_select(0, tidx).cpu().numpy()
+        ms = np.zeros_like(ws)
+        for t in range(steps):
+            oracle.step_flat(gs[t], ws, ms, spec.lr, spec.momentum, spec.weight_decay, spec.nesterov)
+        _say(f"  {spec.name}: {idx.size} sampled elements; W rel err {_rel_err(W[idx], ws):.3g}")
+        assert _bits_equal(W[idx], ws), f"{spec.name}: W mismatch"
+        assert _bits_equal(M[idx], ms), f"{spec.name}: M mismatch"
+        # untouched arena padding stays zero
+        pad = np.ones(W.size, bool)
+        for o, n in zip(job.offsets, spec.key_elems):
+            pad[o:o + n] = False
+        assert not W[pad].any() and not M[pad].any()
+        job.destroy()
+    del grads
+    torch.cuda.empty_cache()

@@ -1,0 +1,200 @@
+"""Host-side checks of the HIP library (no GPU needed).
+
+The chunk schedule is pure host code exported through the C interface; it
+is checked for exact coverage of every element, alignment, small-key
+bundling, refinement and the LPT balance bound.  The library must export
+every function the header declares, and calls that fail argument checks
+must return their error code before touching the GPU.
+"""
+
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1805_07891_amd import phub, workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "phub.h")
+SEG_COST = 4096
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(phub.DEFAULT_LIB):
+        from paper_1805_07891_amd import build
+        build.build()
+    return phub.load()
+
+
+def test_header_symbols_are_exported(lib):
+    with open(HEADER) as f:
+        text = f.read()
+    declared = set(re.findall(r"^\s*(?:int|const char \*)\s*(phub_\w+)\s*\(", text, re.M))
+    assert declared, "no declarations parsed"
+    assert declared == set(phub.EXPORTED)
+    for name in declared:
+        assert hasattr(lib.lib, name), name
+
+
+def _check_plan(lib, n_workers, key_elems, chunk_bytes, groups, min_items=0):
+    segs, gb, gc, item = lib.phub_plan_build(n_workers, key_elems, chunk_bytes, groups, min_items)
+    used = len(gb) - 1
+    assert gb[0] == 0 and gb[-1] == len(segs)
+    assert all(b >= a for a, b in zip(gb, gb[1:]))
+    assert used <= groups
+    assert all(gb[g + 1] > gb[g] for g in range(used)), "a workgroup without work"
+    # coverage: every element of every key exactly once
+    covered = [np.zeros(n, dtype=np.int8) for n in key_elems]
+    for key, count, off in segs:
+        assert count >= 1 and off >= 0 and off + count <= key_elems[key]
+        assert off % 4 == 0, "segment start breaks 16-byte alignment"
+        assert count <= item
+        covered[key][off:off + count] += 1
+    for k, c in enumerate(covered):
+        assert c.size == 0 or (c.min() == 1 and c.max() == 1), f"key {k} not covered exactly once"
+    # costs add up
+    per_elem = (n_workers + 4) * 4
+    expect_total = sum(c * per_elem + SEG_COST for _, c, _ in segs)
+    assert sum(gc) == expect_total
+    for g in range(used):
+        seg_cost = sum(segs[i][1] * per_elem + SEG_COST for i in range(gb[g], gb[g + 1]))
+        assert gc[g] == seg_cost
+        # segments of a workgroup in key, then offset, order
+        keys = [(segs[i][0], segs[i][2]) for i in range(gb[g], gb[g + 1])]
+        assert keys == sorted(keys)
+    return segs, gb, gc, item
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_NAMES)
+@pytest.mark.parametrize("groups", [1, 7, 256, 1 << 30])
+def test_plan_covers_workloads(lib, name, groups):
+    for j in workloads.workload(name).jobs:
+        _check_plan(lib, j.num_workers, j.key_elems, j.chunk_bytes, groups, min_items=512)
+
+
+EDGE_SIZES = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 1023, 1024, 1025, 8191, 8192, 8193, 2 * 8192 + 3, 0]
+
+
+@pytest.mark.parametrize("chunk_bytes", [16, 48, 4096, 32768, 1 << 22])
+@pytest.mark.parametrize("groups", [1, 3, 64])
+def test_plan_edge_shapes(lib, chunk_bytes, groups):
+    _check_plan(lib, 3, EDGE_SIZES, chunk_bytes, groups)
+
+
+def test_plan_bundles_small_keys(lib):
+    # 100 keys of 100 elements with 8192-element chunks: bundles of <= 81 keys
+    keys = [100] * 100
+    segs, gb, gc, item = _check_plan(lib, 4, keys, 32768, 1 << 30)
+    assert len(gb) - 1 == 2  # two items: 81 keys and 19 keys
+    sizes = sorted(gb[g + 1] - gb[g] for g in range(2))
+    assert sizes == [19, 81]
+
+
+def test_plan_bundle_does_not_span_a_large_key(lib):
+    keys = [10, 10, 20000, 10]
+    segs, gb, gc, item = _check_plan(lib, 2, keys, 32768, 1 << 30)
+    # items: {0,1}, three chunks of key 2, {3}
+    assert len(gb) - 1 == 5
+
+
+def test_plan_refines_to_reach_min_items(lib):
+    keys = [8192 * 4]
+    _, gb, _, item = _check_plan(lib, 2, keys, 32768, 1 << 30, min_items=16)
+    assert item == 2048 and len(gb) - 1 == 16
+    # never below 1024 elements
+    _, gb, _, item = _check_plan(lib, 2, keys, 32768, 1 << 30, min_items=10 ** 6)
+    assert item == 1024 and len(gb) - 1 == 32
+    # min_items 0: chunks as given
+    _, gb, _, item = _check_plan(lib, 2, keys, 32768, 1 << 30, min_items=0)
+    assert item == 8192 and len(gb) - 1 == 4
+
+
+def test_plan_one_item_per_group_is_in_decreasing_cost(lib):
+    keys = [5000, 9000, 300, 20000, 7]
+    segs, gb, gc, item = _check_plan(lib, 4, keys, 32768, 1 << 30)
+    assert gc == sorted(gc, reverse=True)
+
+
+def _lpt_opt_bruteforce(costs, groups):
+    best = None
+    for assign in itertools.product(range(groups), repeat=len(costs)):
+        loads = [0] * groups
+        for c, g in zip(costs, assign):
+            loads[g] += c
+        m = max(loads)
+        best = m if best is None else min(best, m)
+    return best
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_lpt_within_graham_bound(lib, seed):
+    rng = np.random.default_rng(seed)
+    groups = int(rng.integers(2, 4))
+    # keys of 1024..3072 elements with 1024-element chunks: every key is at
+    # least one chunk, so nothing is bundled and each chunk is one item
+    chunk = 1024
+    keys, n_items = [], 0
+    while True:
+        n = int(rng.choice([1024, 1536, 2048, 2560, 3072]))
+        c = -(-n // chunk)
+        if n_items + c > 9:
+            break
+        keys.append(n)
+        n_items += c
+    assert n_items > groups
+    segs, gb, gc, item = _check_plan(lib, 2, keys, chunk * 4, groups)
+    assert len(segs) == n_items
+    costs = [c * (2 + 4) * 4 + SEG_COST for _, c, _ in segs]
+    opt = _lpt_opt_bruteforce(costs, groups)
+    assert max(gc) <= (4 / 3 - 1 / (3 * groups)) * opt + 1e-9
+
+
+@pytest.mark.parametrize("name", ["resnet50", "alexnet", "resnet269"])
+def test_plan_list_scheduling_bound_on_workloads(lib, name):
+    # any list schedule: makespan <= total / G + largest item; an item holds
+    # at most `item` elements in at most item / (smallest key) segments
+    j = workloads.workload(name).jobs[0]
+    G = 256
+    segs, gb, gc, item = _check_plan(lib, j.num_workers, j.key_elems, j.chunk_bytes, G)
+    max_segs = -(-item // min(j.key_elems))
+    largest = item * (j.num_workers + 4) * 4 + SEG_COST * max_segs
+    assert max(gc) <= sum(gc) / G + largest
+
+
+@pytest.mark.parametrize("args", [
+    dict(num_workers=0), dict(num_workers=4097), dict(chunk_bytes=0), dict(chunk_bytes=8),
+    dict(chunk_bytes=40), dict(chunk_bytes=(1 << 30) + 16), dict(key_elems=[5, -1]),
+    dict(key_elems=[1 << 40]), dict(groups=0), dict(min_items=-1),
+])
+def test_plan_rejects_bad_arguments(lib, args):
+    a = dict(num_workers=2, key_elems=[5, 9], chunk_bytes=32768, groups=4, min_items=0)
+    a.update(args)
+    with pytest.raises(phub.PhubError) as e:
+        lib.phub_plan_count(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["groups"],
+                            a["min_items"])
+    assert e.value.code == phub.PHUB_EINVAL
+    assert lib.last_error()
+
+
+def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
+    for kw in [dict(num_workers=0), dict(chunk_bytes=20), dict(lr=float("nan")),
+               dict(momentum=float("inf"))]:
+        a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
+                 weight_decay=1e-4, nesterov=True)
+        a.update(kw)
+        rc, h = lib.phub_init(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["lr"],
+                              a["momentum"], a["weight_decay"], a["nesterov"], check=False)
+        assert rc == phub.PHUB_EINVAL and h is None, kw
+
+
+def test_calls_on_a_dead_handle_return_estate(lib):
+    for fn in (lambda: lib.phub_step(None, check=False),
+               lambda: lib.phub_step(12345678, check=False),
+               lambda: lib.phub_push(None, 0, 0, 0, check=False),
+               lambda: lib.phub_sync(None, check=False),
+               lambda: lib.phub_destroy(None, check=False)):
+        assert fn() == phub.PHUB_ESTATE
+    assert "live job" in lib.last_error()
