@@ -82,6 +82,33 @@ int phub_init(phub_job **out, int num_workers, int num_keys, const int64_t *key_
               int64_t chunk_bytes, float lr, float momentum, float weight_decay,
               int nesterov, void *hip_stream);
 
+/* Chunk-to-wave schedules (section 3.2.4; see the schedule section below). */
+enum phub_schedule {
+    PHUB_SCHEDULE_SPLIT = 0, /* contiguous, exactly balanced runs of chunks */
+    PHUB_SCHEDULE_LPT = 1    /* the paper's balanced partition of chunks (default) */
+};
+
+/* Optional settings of phub_init_ex. */
+typedef struct phub_options {
+    int schedule;           /* a phub_schedule value */
+    int64_t resident_bytes; /* bytes of W plus M, from the start of the arenas
+                               (key order), read and written with the
+                               cache-allocating policy so that they can stay in
+                               the GPU's memory-side cache between steps (the
+                               paper's cached model, section 4.5); the rest
+                               streams non-temporally.  -1 keeps the default
+                               (0).  Results do not depend on it. */
+} phub_options;
+
+/*
+ * phub_init_ex - phub_init with options (NULL means the defaults: LPT
+ * schedule, no resident bytes).  Errors as phub_init, plus PHUB_EINVAL for
+ * an unknown schedule or resident_bytes < -1.
+ */
+int phub_init_ex(phub_job **out, int num_workers, int num_keys, const int64_t *key_elems,
+                 int64_t chunk_bytes, float lr, float momentum, float weight_decay,
+                 int nesterov, void *hip_stream, const phub_options *options);
+
 /*
  * phub_set_weights - load key `key`'s master weights from `src` (n_k fp32
  * values, device or host memory) and reset its momentum to zero.  The copy
@@ -153,8 +180,8 @@ int phub_get_stream(phub_job *job, void **hip_stream);
 
 /*
  * phub_job_info - launch shape of the job's step: the number of workgroups
- * of one launch, the threads per workgroup and the number of work segments
- * in the schedule.  Any output may be NULL.
+ * of one launch (0 if every key is empty), the threads per workgroup and the
+ * number of work segments in the schedule.  Any output may be NULL.
  */
 int phub_job_info(phub_job *job, int *workgroups, int *threads_per_group, int64_t *segments);
 
@@ -174,51 +201,59 @@ const char *phub_last_error(void);
  * runs it; it is exported so that its coverage and balance can be checked
  * without a GPU.
  *
- * Keys are cut into chunks of chunk_bytes/4 elements, the last one partial
- * (section 3.2.3's virtual keys).  Keys smaller than a chunk are bundled, in
- * key order, into items of at most one chunk (a run of small keys is not
- * bundled across a larger key).  While there are fewer than min_items
- * items, the chunk is halved (not below 1024 elements) so that every
- * compute unit gets work; the result of a step does not depend on the cut.
- * Items are assigned to at most num_groups workgroups by the
- * longest-processing-time-first rule (largest item first, each to the least
- * loaded workgroup, lowest index on ties), a 4/3-approximate balanced
- * partition like the paper's (section 3.2.4).  Item cost is the bytes it
- * moves, (N + 4) * 4 per element, plus 4096 per segment.  With num_groups
- * at least the number of items, workgroup g holds the g-th largest item,
- * and the GPU's in-order dispatch of workgroups performs the same rule
- * online.
+ * The unit that plays a PHub core is one wave (64 lanes) of the fused
+ * kernel; the kernel runs one persistent workgroup per compute unit, and
+ * each wave walks its own bin: a list of segments fixed at initialisation.
+ * Keys are cut into chunks of chunk_bytes/4 elements (section 3.2.3's
+ * virtual keys), the last one of a key partial.
+ *
+ * PHUB_SCHEDULE_SPLIT: the keys, in key order, are dealt to the num_bins
+ *   bins as contiguous runs of equal length (to within one 16-byte float4),
+ *   each run cut into segments at chunk boundaries.  On a GPU a chunk can be
+ *   split on any 16-byte boundary, so the load is balanced exactly.  All
+ *   num_bins bins are kept (an empty run is an empty bin); min_items is
+ *   ignored.
+ * PHUB_SCHEDULE_LPT: chunks are indivisible items, as in the paper.  Keys
+ *   smaller than a chunk are bundled, in key order, into items of at most one
+ *   chunk (a run of small keys is not bundled across a larger key).  While
+ *   there are fewer than min_items items, the chunk is halved (not below
+ *   1024 elements).  Items go to the bins by the longest-processing-time-
+ *   first rule (largest item first, each to the least loaded bin, lowest
+ *   index on ties), a 4/3-approximate balanced partition like the paper's.
+ *   Bins that get no item are dropped.
+ * Item and segment cost is the bytes moved, (N + 4) * 4 per element, plus
+ * 4096 per segment.  The result of a step depends on neither schedule nor
+ * chunk size.  phub_init uses one bin per wave of its launch (one workgroup
+ * of 4 waves per compute unit) and, for LPT, min_items = 32 per bin.
  * ------------------------------------------------------------------------ */
 
-/* One contiguous run of one key handled by one workgroup. */
+/* One contiguous run of one key handled by one wave. */
 typedef struct phub_segment {
     int32_t key;    /* key index */
     int32_t count;  /* number of elements, >= 1 */
-    int64_t offset; /* index of the first element within the key */
+    int64_t offset; /* index of the first element within the key, a multiple of 4 */
 } phub_segment;
 
 /*
  * phub_plan_count - sizes of the schedule for these arguments (same meaning
- * and checks as phub_init; num_groups >= 1 caps the workgroups, min_items
- * >= 0 is the refinement target above): *num_segments and *groups_used
- * (<= num_groups; workgroups with no work are dropped), and *item_elems
- * (may be NULL), the chunk size after refinement.  Errors: PHUB_EINVAL.
+ * and checks as phub_init; schedule a phub_schedule value; num_bins >= 1;
+ * min_items >= 0): *num_segments, *bins_used and *item_elems (the chunk
+ * size after refinement).  Any output may be NULL.  Errors: PHUB_EINVAL.
  */
 int phub_plan_count(int num_workers, int num_keys, const int64_t *key_elems,
-                    int64_t chunk_bytes, int num_groups, int min_items,
-                    int64_t *num_segments, int *groups_used, int64_t *item_elems);
+                    int64_t chunk_bytes, int schedule, int num_bins, int min_items,
+                    int64_t *num_segments, int *bins_used, int64_t *item_elems);
 
 /*
  * phub_plan_build - the schedule itself, into caller arrays sized by
- * phub_plan_count: segments[num_segments], grouped by workgroup;
- * group_begin[groups_used + 1] with workgroup g owning segments
- * group_begin[g] .. group_begin[g+1]-1 (in key, then offset, order);
- * group_cost[groups_used] (may be NULL) the cost assigned to each workgroup.
- * Errors: PHUB_EINVAL.
+ * phub_plan_count: segments[num_segments], grouped by bin;
+ * bin_begin[bins_used + 1], bin b owning segments bin_begin[b] ..
+ * bin_begin[b+1]-1 in key, then offset, order; bin_cost[bins_used] (may be
+ * NULL) the cost of each bin.  Errors: PHUB_EINVAL.
  */
 int phub_plan_build(int num_workers, int num_keys, const int64_t *key_elems,
-                    int64_t chunk_bytes, int num_groups, int min_items,
-                    phub_segment *segments, int64_t *group_begin, int64_t *group_cost);
+                    int64_t chunk_bytes, int schedule, int num_bins, int min_items,
+                    phub_segment *segments, int64_t *bin_begin, int64_t *bin_cost);
 
 #ifdef __cplusplus
 }

@@ -24,18 +24,18 @@
 #include "phub.h"
 #include "plan.hpp"
 
-#ifndef PHUB_BLOCK_THREADS
-#define PHUB_BLOCK_THREADS 256
-#endif
-// Cap on workgroups per compute unit in the schedule; 0 means one workgroup
-// per item (the dispatcher then runs the items largest first).
+// Workgroups per compute unit of the persistent launch.
 #ifndef PHUB_GROUPS_PER_CU
-#define PHUB_GROUPS_PER_CU 0
+#define PHUB_GROUPS_PER_CU 1
 #endif
-
-static_assert(PHUB_BLOCK_THREADS >= 64 && PHUB_BLOCK_THREADS <= phub::kMaxBlockThreads &&
-                  PHUB_BLOCK_THREADS % 64 == 0,
-              "block size must be a multiple of the wave size");
+// Default bytes of W plus M (from the start of the arenas) accessed with the
+// cache-allocating policy so that they can stay in the memory-side cache
+// between steps; the rest streams non-temporally.
+#ifndef PHUB_RESIDENT_BYTES
+#define PHUB_RESIDENT_BYTES 0
+#endif
+// The LPT schedule refines chunks until there are this many items per bin.
+constexpr int kLptItemsPerBin = 32;
 
 namespace {
 
@@ -77,14 +77,16 @@ struct phub_job {
     hipStream_t stream = nullptr;
     bool own_stream = false;
 
-    int groups = 0;
-    int block = PHUB_BLOCK_THREADS;
+    int schedule = phub::kScheduleLpt;
+    int groups = 0;  // workgroups of one launch
+    int bins = 0;    // waves with a segment list (groups * waves per workgroup)
     int64_t num_segments = 0;
+    int64_t resident_elems = 0;
 
     float* weights = nullptr;
     float* moments = nullptr;
     phub::DevSegment* d_segments = nullptr;
-    int64_t* d_group_begin = nullptr;
+    int64_t* d_bin_begin = nullptr;
     const float** d_grads = nullptr;
 
     std::vector<const float*> grads;  // host table, [key * N + worker]
@@ -125,7 +127,7 @@ bool is_live(const phub_job* j) {
 
 void release(phub_job* j) {
     if (j->d_grads) (void)hipFree(j->d_grads);
-    if (j->d_group_begin) (void)hipFree(j->d_group_begin);
+    if (j->d_bin_begin) (void)hipFree(j->d_bin_begin);
     if (j->d_segments) (void)hipFree(j->d_segments);
     if (j->moments) (void)hipFree(j->moments);
     if (j->weights) (void)hipFree(j->weights);
@@ -193,47 +195,54 @@ extern "C" {
 const char* phub_last_error(void) { return g_error.c_str(); }
 
 int phub_plan_count(int num_workers, int num_keys, const int64_t* key_elems, int64_t chunk_bytes,
-                    int num_groups, int min_items, int64_t* num_segments, int* groups_used,
-                    int64_t* item_elems) {
+                    int schedule, int num_bins, int min_items, int64_t* num_segments,
+                    int* bins_used, int64_t* item_elems) {
     phub::Plan plan;
     std::string err;
     try {
-        err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, num_groups, min_items,
-                               &plan);
+        err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, schedule, num_bins,
+                               min_items, &plan);
     } catch (const std::bad_alloc&) {
         return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
     }
     if (!err.empty()) return fail(PHUB_EINVAL, "%s", err.c_str());
     if (num_segments) *num_segments = int64_t(plan.segments.size());
-    if (groups_used) *groups_used = plan.groups_used();
+    if (bins_used) *bins_used = plan.bins_used();
     if (item_elems) *item_elems = plan.item_elems;
     return PHUB_OK;
 }
 
 int phub_plan_build(int num_workers, int num_keys, const int64_t* key_elems, int64_t chunk_bytes,
-                    int num_groups, int min_items, phub_segment* segments, int64_t* group_begin,
-                    int64_t* group_cost) {
+                    int schedule, int num_bins, int min_items, phub_segment* segments,
+                    int64_t* bin_begin, int64_t* bin_cost) {
     phub::Plan plan;
     std::string err;
     try {
-        err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, num_groups, min_items,
-                               &plan);
+        err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, schedule, num_bins,
+                               min_items, &plan);
     } catch (const std::bad_alloc&) {
         return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
     }
     if (!err.empty()) return fail(PHUB_EINVAL, "%s", err.c_str());
-    if ((!segments && !plan.segments.empty()) || !group_begin)
+    if ((!segments && !plan.segments.empty()) || !bin_begin)
         return fail(PHUB_EINVAL, "output arrays are NULL");
     for (size_t i = 0; i < plan.segments.size(); ++i)
         segments[i] = {plan.segments[i].key, plan.segments[i].count, plan.segments[i].offset};
-    std::copy(plan.group_begin.begin(), plan.group_begin.end(), group_begin);
-    if (group_cost) std::copy(plan.group_cost.begin(), plan.group_cost.end(), group_cost);
+    std::copy(plan.bin_begin.begin(), plan.bin_begin.end(), bin_begin);
+    if (bin_cost) std::copy(plan.bin_cost.begin(), plan.bin_cost.end(), bin_cost);
     return PHUB_OK;
 }
 
 int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_elems,
               int64_t chunk_bytes, float lr, float momentum, float weight_decay, int nesterov,
               void* hip_stream) {
+    return phub_init_ex(out, num_workers, num_keys, key_elems, chunk_bytes, lr, momentum,
+                        weight_decay, nesterov, hip_stream, nullptr);
+}
+
+int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* key_elems,
+                 int64_t chunk_bytes, float lr, float momentum, float weight_decay, int nesterov,
+                 void* hip_stream, const phub_options* options) {
     if (!out) return fail(PHUB_EINVAL, "out is NULL");
     *out = nullptr;
     {
@@ -242,6 +251,17 @@ int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_
     }
     if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
         return fail(PHUB_EINVAL, "lr, momentum and weight_decay must be finite");
+    int schedule = phub::kScheduleLpt;
+    int64_t resident_bytes = PHUB_RESIDENT_BYTES;
+    if (options) {
+        if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
+            return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
+        if (options->resident_bytes < -1)
+            return fail(PHUB_EINVAL, "resident_bytes must be >= -1, got %lld",
+                        (long long)options->resident_bytes);
+        schedule = options->schedule;
+        if (options->resident_bytes >= 0) resident_bytes = options->resident_bytes;
+    }
 
     phub_job* j = new (std::nothrow) phub_job;
     if (!j) return fail(PHUB_ENOMEM, "host allocation of the job failed");
@@ -282,11 +302,12 @@ int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_
 
     phub::Plan plan;
     {
-        const int64_t cap = PHUB_GROUPS_PER_CU > 0 ? int64_t(cus) * PHUB_GROUPS_PER_CU : (1 << 30);
+        const int groups = cus * PHUB_GROUPS_PER_CU;
+        const int bins = groups * (phub::kBlockThreads / 64);
         std::string err;
         try {
-            err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, int(cap), 2 * cus,
-                                   &plan);
+            err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, schedule, bins,
+                                   kLptItemsPerBin * bins, &plan);
         } catch (const std::bad_alloc&) {
             delete j;
             return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
@@ -295,9 +316,14 @@ int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_
             delete j;
             return fail(PHUB_EINVAL, "%s", err.c_str());
         }
+        // every wave of the grid reads its bin: pad dropped bins as empty
+        while (plan.bin_begin.size() < size_t(bins) + 1) plan.bin_begin.push_back(plan.bin_begin.back());
+        j->groups = plan.segments.empty() ? 0 : groups;
+        j->bins = bins;
     }
-    j->groups = plan.groups_used();
+    j->schedule = schedule;
     j->num_segments = int64_t(plan.segments.size());
+    j->resident_elems = resident_bytes / 8;  // W and M, 4 bytes each
 
 #define PHUB_TRY(call, what)                 \
     do {                                     \
@@ -332,10 +358,10 @@ int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_
             dseg[i] = {j->arena_offset[s.key] + s.offset, s.offset, s.key, s.count, 0};
         }
         const size_t seg_bytes = std::max<size_t>(dseg.size(), 1) * sizeof(phub::DevSegment);
-        const size_t gb_bytes = plan.group_begin.size() * sizeof(int64_t);
+        const size_t gb_bytes = plan.bin_begin.size() * sizeof(int64_t);
         const size_t tab_bytes = j->grads.size() * sizeof(const float*);
         if (hipMalloc(&j->d_segments, seg_bytes) != hipSuccess ||
-            hipMalloc(&j->d_group_begin, gb_bytes) != hipSuccess ||
+            hipMalloc(&j->d_bin_begin, gb_bytes) != hipSuccess ||
             hipMalloc(&j->d_grads, tab_bytes) != hipSuccess) {
             (void)hipGetLastError();
             rc = fail(PHUB_ENOMEM, "device allocation of the schedule failed");
@@ -345,9 +371,8 @@ int phub_init(phub_job** out, int num_workers, int num_keys, const int64_t* key_
             PHUB_TRY(hipMemcpy(j->d_segments, dseg.data(), dseg.size() * sizeof(phub::DevSegment),
                                hipMemcpyHostToDevice),
                      "hipMemcpy(schedule)");
-        PHUB_TRY(hipMemcpy(j->d_group_begin, plan.group_begin.data(), gb_bytes,
-                           hipMemcpyHostToDevice),
-                 "hipMemcpy(group table)");
+        PHUB_TRY(hipMemcpy(j->d_bin_begin, plan.bin_begin.data(), gb_bytes, hipMemcpyHostToDevice),
+                 "hipMemcpy(bin table)");
         for (int i = 0; i < kStageSlots; ++i) {
             if (hipHostMalloc(reinterpret_cast<void**>(&j->stage[i]), tab_bytes,
                               hipHostMallocDefault) != hipSuccess) {
@@ -429,7 +454,7 @@ int phub_step(phub_job* j) {
     if (j->groups > 0) {
         phub::StepParams p;
         p.segments = j->d_segments;
-        p.group_begin = j->d_group_begin;
+        p.bin_begin = j->d_bin_begin;
         p.grads = j->d_grads;
         p.weights = j->weights;
         p.moments = j->moments;
@@ -437,7 +462,8 @@ int phub_step(phub_job* j) {
         p.mu = j->mu;
         p.wd = j->wd;
         p.num_workers = j->num_workers;
-        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->groups, j->block, j->stream);
+        p.resident_elems = j->resident_elems;
+        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->groups, j->stream);
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
     }
     std::fill(j->pushed.begin(), j->pushed.end(), 0);
@@ -480,7 +506,7 @@ int phub_get_stream(phub_job* j, void** hip_stream) {
 int phub_job_info(phub_job* j, int* workgroups, int* threads_per_group, int64_t* segments) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     if (workgroups) *workgroups = j->groups;
-    if (threads_per_group) *threads_per_group = j->block;
+    if (threads_per_group) *threads_per_group = phub::kBlockThreads;
     if (segments) *segments = j->num_segments;
     return PHUB_OK;
 }

@@ -54,7 +54,8 @@ class TorchJob:
     """
 
     def __init__(self, spec: Job, device, stream=None, chunk_bytes: Optional[int] = None,
-                 lib: Optional[_phub.Library] = None):
+                 lib: Optional[_phub.Library] = None, schedule: Optional[int] = None,
+                 resident_bytes: Optional[int] = None):
         import torch
         self.torch = torch
         self.spec = spec
@@ -66,7 +67,8 @@ class TorchJob:
         with torch.cuda.device(self.device):
             self.handle = self.lib.phub_init(spec.num_workers, spec.key_elems, self.chunk_bytes,
                                              spec.lr, spec.momentum, spec.weight_decay,
-                                             spec.nesterov, self.stream.cuda_stream)
+                                             spec.nesterov, self.stream.cuda_stream,
+                                             schedule=schedule, resident_bytes=resident_bytes)
         self._ptr_arrays: List = [None] * spec.num_workers
         self._grad_refs: List = [None] * spec.num_workers
 

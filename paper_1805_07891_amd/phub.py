@@ -27,10 +27,14 @@ PHUB_ESTATE = -5
 STATUS_NAMES = {0: "PHUB_OK", -1: "PHUB_EINVAL", -2: "PHUB_ENOTREADY", -3: "PHUB_ENOMEM",
                 -4: "PHUB_EHIP", -5: "PHUB_ESTATE"}
 
+PHUB_SCHEDULE_SPLIT = 0
+PHUB_SCHEDULE_LPT = 1
+
 # Every symbol the header declares.
-EXPORTED = ("phub_init", "phub_set_weights", "phub_push", "phub_push_keys", "phub_step",
-            "phub_pull", "phub_get_state", "phub_sync", "phub_get_stream", "phub_job_info",
-            "phub_destroy", "phub_last_error", "phub_plan_count", "phub_plan_build")
+EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_push_keys",
+            "phub_step", "phub_pull", "phub_get_state", "phub_sync", "phub_get_stream",
+            "phub_job_info", "phub_destroy", "phub_last_error", "phub_plan_count",
+            "phub_plan_build")
 
 
 class PhubError(RuntimeError):
@@ -41,6 +45,10 @@ class PhubError(RuntimeError):
 
 class PhubSegment(ctypes.Structure):
     _fields_ = [("key", ctypes.c_int32), ("count", ctypes.c_int32), ("offset", ctypes.c_int64)]
+
+
+class PhubOptions(ctypes.Structure):
+    _fields_ = [("schedule", ctypes.c_int), ("resident_bytes", ctypes.c_int64)]
 
 
 class Library:
@@ -55,6 +63,8 @@ class Library:
         pp = ctypes.POINTER(ctypes.c_void_p)
         sig = {
             "phub_init": ([pp, i32, i32, vp, i64, f32, f32, f32, i32, vp], i32),
+            "phub_init_ex": ([pp, i32, i32, vp, i64, f32, f32, f32, i32, vp,
+                              ctypes.POINTER(PhubOptions)], i32),
             "phub_set_weights": ([vp, i32, vp], i32),
             "phub_push": ([vp, i32, i32, vp], i32),
             "phub_push_keys": ([vp, i32, i32, vp, vp], i32),
@@ -66,9 +76,9 @@ class Library:
             "phub_job_info": ([vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64)], i32),
             "phub_destroy": ([vp], i32),
             "phub_last_error": ([], ctypes.c_char_p),
-            "phub_plan_count": ([i32, i32, vp, i64, i32, i32, ctypes.POINTER(i64),
+            "phub_plan_count": ([i32, i32, vp, i64, i32, i32, i32, ctypes.POINTER(i64),
                                  ctypes.POINTER(i32), ctypes.POINTER(i64)], i32),
-            "phub_plan_build": ([i32, i32, vp, i64, i32, i32, vp, vp, vp], i32),
+            "phub_plan_build": ([i32, i32, vp, i64, i32, i32, i32, vp, vp, vp], i32),
         }
         for name, (args, res) in sig.items():
             fn = getattr(lib, name)
@@ -87,14 +97,22 @@ class Library:
     # -- job lifecycle -----------------------------------------------------
     def phub_init(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
                   lr: float, momentum: float, weight_decay: float, nesterov: bool,
-                  hip_stream: Optional[int] = None, check: bool = True):
-        """Returns the job handle (an int), or (rc, None) with check=False on error."""
+                  hip_stream: Optional[int] = None, check: bool = True,
+                  schedule: Optional[int] = None, resident_bytes: Optional[int] = None):
+        """Returns the job handle (an int), or (rc, None) with check=False on
+        error.  With ``schedule`` or ``resident_bytes`` given, calls
+        phub_init_ex with those options."""
         elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
         out = ctypes.c_void_p()
-        rc = self.lib.phub_init(ctypes.byref(out), int(num_workers), len(key_elems),
-                                ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes),
-                                float(lr), float(momentum), float(weight_decay),
-                                int(bool(nesterov)), hip_stream)
+        args = (ctypes.byref(out), int(num_workers), len(key_elems),
+                ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes), float(lr), float(momentum),
+                float(weight_decay), int(bool(nesterov)), hip_stream)
+        if schedule is None and resident_bytes is None:
+            rc = self.lib.phub_init(*args)
+        else:
+            opts = PhubOptions(PHUB_SCHEDULE_LPT if schedule is None else int(schedule),
+                               -1 if resident_bytes is None else int(resident_bytes))
+            rc = self.lib.phub_init_ex(*args, ctypes.byref(opts))
         if rc != 0:
             self._check(rc, check)
             return rc, None
@@ -148,30 +166,32 @@ class Library:
 
     # -- schedule (host only) ----------------------------------------------
     def phub_plan_count(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
-                        num_groups: int, min_items: int = 0):
+                        num_bins: int, min_items: int = 0, schedule: int = PHUB_SCHEDULE_SPLIT):
         elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
         nseg, used, item = ctypes.c_int64(), ctypes.c_int(), ctypes.c_int64()
         self._check(self.lib.phub_plan_count(int(num_workers), len(key_elems),
                                              ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes),
-                                             int(num_groups), int(min_items), ctypes.byref(nseg),
-                                             ctypes.byref(used), ctypes.byref(item)), True)
+                                             int(schedule), int(num_bins), int(min_items),
+                                             ctypes.byref(nseg), ctypes.byref(used),
+                                             ctypes.byref(item)), True)
         return nseg.value, used.value, item.value
 
     def phub_plan_build(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
-                        num_groups: int, min_items: int = 0):
-        """Returns (segments as a list of (key, count, offset), group_begin,
-        group_cost, item_elems)."""
-        nseg, used, item = self.phub_plan_count(num_workers, key_elems, chunk_bytes, num_groups,
-                                                min_items)
+                        num_bins: int, min_items: int = 0, schedule: int = PHUB_SCHEDULE_SPLIT):
+        """Returns (segments as a list of (key, count, offset), bin_begin,
+        bin_cost, item_elems)."""
+        nseg, used, item = self.phub_plan_count(num_workers, key_elems, chunk_bytes, num_bins,
+                                                min_items, schedule)
         elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
         segs = (PhubSegment * max(nseg, 1))()
-        gb = (ctypes.c_int64 * (used + 1))()
-        gc = (ctypes.c_int64 * max(used, 1))()
+        bb = (ctypes.c_int64 * (used + 1))()
+        bc = (ctypes.c_int64 * max(used, 1))()
         self._check(self.lib.phub_plan_build(int(num_workers), len(key_elems),
                                              ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes),
-                                             int(num_groups), int(min_items), segs, gb, gc), True)
+                                             int(schedule), int(num_bins), int(min_items), segs,
+                                             bb, bc), True)
         seg_list = [(segs[i].key, segs[i].count, segs[i].offset) for i in range(nseg)]
-        return seg_list, list(gb), list(gc[:used]), item
+        return seg_list, list(bb), list(bc[:used]), item
 
 
 def pointer_array(ptrs: Sequence[int]):

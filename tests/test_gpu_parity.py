@@ -54,12 +54,13 @@ def _rel_err(x, ref):
 
 def run_small_case(torch, dev, lib, n_workers, key_elems, steps=2, chunk_bytes=32768,
                    lr=0.1, mu=0.9, wd=1e-4, nesterov=True, seed=0, push="keys",
-                   reuse_buffers=False, stream=None):
+                   reuse_buffers=False, stream=None, schedule=None, resident_bytes=None):
     """Runs `steps` steps on the GPU and in the oracle; returns the job and
     per-step (gpu W, gpu M, oracle W, oracle M) lists per key."""
     spec = Job("case", n_workers, tuple(int(n) for n in key_elems), chunk_elems=chunk_bytes // 4,
                lr=lr, momentum=mu, weight_decay=wd, nesterov=nesterov, sigma_g=1e-2)
-    job = TorchJob(spec, dev, stream=stream, chunk_bytes=chunk_bytes, lib=lib)
+    job = TorchJob(spec, dev, stream=stream, chunk_bytes=chunk_bytes, lib=lib, schedule=schedule,
+                   resident_bytes=resident_bytes)
     offs, total = key_offsets(spec.key_elems)
     rng = np.random.default_rng(seed)
     w0 = np.zeros(total, np.float32)
@@ -173,6 +174,19 @@ def test_chunk_size_does_not_change_results(lib, torch_dev):
     for wg, mg in outs[1:]:
         for k in range(len(keys)):
             assert _bits_equal(wg[k], outs[0][0][k]) and _bits_equal(mg[k], outs[0][1][k])
+
+
+@pytest.mark.parametrize("schedule", [phub.PHUB_SCHEDULE_SPLIT, phub.PHUB_SCHEDULE_LPT])
+@pytest.mark.parametrize("resident", [0, 4096, 1 << 20, 1 << 40])
+def test_schedule_and_cache_residency_do_not_change_results(lib, torch_dev, schedule, resident):
+    torch, dev = torch_dev
+    keys = [3, 100, 8192 * 3 + 5, 70000, 1, 4096, 333333]
+    for n in (4, 8, 16, 19):
+        _say("schedule", schedule, "resident", resident, "N", n)
+        job, res = run_small_case(torch, dev, lib, n, keys, steps=2, seed=1000 + n,
+                                  schedule=schedule, resident_bytes=resident)
+        assert_parity(res, f"schedule={schedule} resident={resident} N={n}")
+        job.destroy()
 
 
 def test_push_order_and_single_pushes(lib, torch_dev):

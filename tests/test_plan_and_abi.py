@@ -39,19 +39,27 @@ def test_header_symbols_are_exported(lib):
         assert hasattr(lib.lib, name), name
 
 
-def _check_plan(lib, n_workers, key_elems, chunk_bytes, groups, min_items=0):
-    segs, gb, gc, item = lib.phub_plan_build(n_workers, key_elems, chunk_bytes, groups, min_items)
+LPT = phub.PHUB_SCHEDULE_LPT
+SPLIT = phub.PHUB_SCHEDULE_SPLIT
+
+
+def _check_plan(lib, n_workers, key_elems, chunk_bytes, groups, min_items=0, schedule=LPT):
+    segs, gb, gc, item = lib.phub_plan_build(n_workers, key_elems, chunk_bytes, groups, min_items,
+                                             schedule)
     used = len(gb) - 1
     assert gb[0] == 0 and gb[-1] == len(segs)
     assert all(b >= a for a, b in zip(gb, gb[1:]))
     assert used <= groups
-    assert all(gb[g + 1] > gb[g] for g in range(used)), "a workgroup without work"
+    if schedule == LPT:
+        assert all(gb[g + 1] > gb[g] for g in range(used)), "a bin without work"
+    else:
+        assert used == groups
     # coverage: every element of every key exactly once
     covered = [np.zeros(n, dtype=np.int8) for n in key_elems]
     for key, count, off in segs:
         assert count >= 1 and off >= 0 and off + count <= key_elems[key]
         assert off % 4 == 0, "segment start breaks 16-byte alignment"
-        assert count <= item
+        assert count <= chunk_bytes // 4 and (schedule == SPLIT or count <= item)
         covered[key][off:off + count] += 1
     for k, c in enumerate(covered):
         assert c.size == 0 or (c.min() == 1 and c.max() == 1), f"key {k} not covered exactly once"
@@ -69,10 +77,36 @@ def _check_plan(lib, n_workers, key_elems, chunk_bytes, groups, min_items=0):
 
 
 @pytest.mark.parametrize("name", workloads.WORKLOAD_NAMES)
-@pytest.mark.parametrize("groups", [1, 7, 256, 1 << 30])
-def test_plan_covers_workloads(lib, name, groups):
+@pytest.mark.parametrize("groups", [1, 7, 256, 1024])
+@pytest.mark.parametrize("schedule", [LPT, SPLIT])
+def test_plan_covers_workloads(lib, name, groups, schedule):
     for j in workloads.workload(name).jobs:
-        _check_plan(lib, j.num_workers, j.key_elems, j.chunk_bytes, groups, min_items=512)
+        _check_plan(lib, j.num_workers, j.key_elems, j.chunk_bytes, groups, min_items=512,
+                    schedule=schedule)
+
+
+@pytest.mark.parametrize("name", ["tiny", "resnet50", "alexnet", "resnet269"])
+@pytest.mark.parametrize("bins", [1, 5, 1024])
+def test_split_is_balanced_and_contiguous(lib, name, bins):
+    j = workloads.workload(name).jobs[0]
+    segs, bb, bc, item = _check_plan(lib, j.num_workers, j.key_elems, j.chunk_bytes, bins,
+                                     schedule=SPLIT)
+    # every bin holds the same number of float4 slots, to within one
+    slots = [sum((c + 3) // 4 for _, c, _ in segs[bb[b]:bb[b + 1]]) for b in range(bins)]
+    assert max(slots) - min(slots) <= 1
+    # bins are contiguous runs in key order: concatenated, they walk the keys in order
+    flat = [(k, o, c) for k, c, o in segs]
+    for (k0, o0, c0), (k1, o1, c1) in zip(flat, flat[1:]):
+        assert (k1 == k0 and o1 == o0 + c0) or (k1 > k0 and o1 == 0 and o0 + c0 == j.key_elems[k0])
+    # no segment crosses a chunk boundary
+    C = j.chunk_bytes // 4
+    for k, o, c in flat:
+        assert o // C == (o + c - 1) // C
+
+
+def test_split_with_more_bins_than_float4_slots(lib):
+    segs, bb, bc, item = _check_plan(lib, 3, [5, 2, 0, 1], 32768, 64, schedule=SPLIT)
+    assert len(bb) == 65 and sum(1 for b in range(64) if bb[b + 1] > bb[b]) == 4
 
 
 EDGE_SIZES = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 1023, 1024, 1025, 8191, 8192, 8193, 2 * 8192 + 3, 0]
@@ -80,8 +114,9 @@ EDGE_SIZES = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 1023, 1024, 1025, 8191, 8192, 819
 
 @pytest.mark.parametrize("chunk_bytes", [16, 48, 4096, 32768, 1 << 22])
 @pytest.mark.parametrize("groups", [1, 3, 64])
-def test_plan_edge_shapes(lib, chunk_bytes, groups):
-    _check_plan(lib, 3, EDGE_SIZES, chunk_bytes, groups)
+@pytest.mark.parametrize("schedule", [LPT, SPLIT])
+def test_plan_edge_shapes(lib, chunk_bytes, groups, schedule):
+    _check_plan(lib, 3, EDGE_SIZES, chunk_bytes, groups, schedule=schedule)
 
 
 def test_plan_bundles_small_keys(lib):
@@ -167,26 +202,29 @@ def test_plan_list_scheduling_bound_on_workloads(lib, name):
 @pytest.mark.parametrize("args", [
     dict(num_workers=0), dict(num_workers=4097), dict(chunk_bytes=0), dict(chunk_bytes=8),
     dict(chunk_bytes=40), dict(chunk_bytes=(1 << 30) + 16), dict(key_elems=[5, -1]),
-    dict(key_elems=[1 << 40]), dict(groups=0), dict(min_items=-1),
+    dict(key_elems=[1 << 40]), dict(groups=0), dict(min_items=-1), dict(schedule=2),
+    dict(schedule=-1),
 ])
 def test_plan_rejects_bad_arguments(lib, args):
-    a = dict(num_workers=2, key_elems=[5, 9], chunk_bytes=32768, groups=4, min_items=0)
+    a = dict(num_workers=2, key_elems=[5, 9], chunk_bytes=32768, groups=4, min_items=0,
+             schedule=LPT)
     a.update(args)
     with pytest.raises(phub.PhubError) as e:
         lib.phub_plan_count(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["groups"],
-                            a["min_items"])
+                            a["min_items"], a["schedule"])
     assert e.value.code == phub.PHUB_EINVAL
     assert lib.last_error()
 
 
 def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
     for kw in [dict(num_workers=0), dict(chunk_bytes=20), dict(lr=float("nan")),
-               dict(momentum=float("inf"))]:
+               dict(momentum=float("inf")), dict(schedule=7), dict(resident_bytes=-2)]:
         a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
-                 weight_decay=1e-4, nesterov=True)
+                 weight_decay=1e-4, nesterov=True, schedule=None, resident_bytes=None)
         a.update(kw)
         rc, h = lib.phub_init(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["lr"],
-                              a["momentum"], a["weight_decay"], a["nesterov"], check=False)
+                              a["momentum"], a["weight_decay"], a["nesterov"], check=False,
+                              schedule=a["schedule"], resident_bytes=a["resident_bytes"])
         assert rc == phub.PHUB_EINVAL and h is None, kw
 
 
