@@ -91,13 +91,15 @@ enum phub_schedule {
 /* Optional settings of phub_init_ex. */
 typedef struct phub_options {
     int schedule;           /* a phub_schedule value */
-    int64_t resident_bytes; /* bytes of W plus M, from the start of the arenas
-                               (key order), read and written with the
-                               cache-allocating policy so that they can stay in
-                               the GPU's memory-side cache between steps (the
-                               paper's cached model, section 4.5); the rest
-                               streams non-temporally.  -1 keeps the default
-                               (0).  Results do not depend on it. */
+    int64_t resident_bytes; /* a budget in bytes for keeping W and M in the
+                               GPU's memory-side cache between steps (the
+                               paper's cached model, section 4.5): when the
+                               whole W and M arenas (8 bytes per padded
+                               element) fit in it, they are read and written
+                               with the cache-allocating policy; otherwise, and
+                               for 0, they stream non-temporally like the
+                               gradients.  -1 keeps the default (0).  Results
+                               do not depend on it. */
 } phub_options;
 
 /*

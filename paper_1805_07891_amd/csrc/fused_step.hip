@@ -1,8 +1,8 @@
 // Fused aggregate + optimize kernel of the exchange step, for gfx950.
 //
 // One wave plays the role of one PHub core (paper, section 3.2.4): it walks
-// the list of segments (runs of chunks) the schedule fixed for it at
-// initialisation, and for each element it sums the N workers' gradients
+// the list of chunks the schedule fixed for it at initialisation, and for
+// each element it sums the N workers' gradients
 // (section 3.2.2, "tall" aggregation: one worker takes the same chunk
 // across all gradient arrays) and immediately runs the optimizer on that
 // element (section 3.2.2: the thread that aggregates a chunk also
@@ -16,14 +16,17 @@
 // few waves per CU, each keeping many bytes in flight, rather than with many
 // small workgroups.
 //
-// Memory access: a lane handles U float4 of each array per iteration, the
-// wave's 64 lanes covering U contiguous 1 KB pieces of each of the N + 2
-// arrays, all N * U gradient loads in flight before the first addition.
+// Memory access: a wave's hot loop moves one tile per iteration, 1024
+// elements of each of the N + 2 arrays: a lane loads 4 float4 of each
+// (the wave's 64 lanes cover 4 contiguous 1 KB pieces), all 4 * N gradient
+// loads in flight before the first addition.  Segments are cut on the host
+// into full tiles and a remainder, so the hot loop is straight-line code.
 // Gradients are read once per step and loaded non-temporally.  W and M are
-// read and written non-temporally, except a leading part of the arenas
-// (resident_elems) that uses the default policy so that it can stay in the
-// memory-side cache between steps.  Segment descriptors and per-key
-// gradient pointers are uniform per wave and come through scalar loads.
+// read and written non-temporally, unless the job asks for them to stay in
+// the memory-side cache between steps (RES: default, cache-allocating
+// policy for every W and M access of the launch).  Tile descriptors and
+// per-key gradient pointers are uniform per wave and come through scalar
+// loads, prefetched two tiles ahead.
 //
 // Arithmetic (no MFMA: the work is elementwise and HBM-bound): the sum is a
 // left fold in ascending worker index, plain fp32 additions; then four
@@ -46,18 +49,6 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 namespace {
 
 constexpr int kWavesPerBlock = kBlockThreads / 64;
-
-// float4 per lane per array and iteration: all N * U gradient loads of a
-// lane are live at once (up to 16 * 4 * 4 = 256 VGPRs of data at N = 16,
-// within the 512 a lane may use at one wave per SIMD).
-template <int NW>
-constexpr int vec_per_lane() {
-#if defined(PHUB_VEC_PER_LANE) && PHUB_VEC_PER_LANE > 0
-    return PHUB_VEC_PER_LANE;
-#else
-    return 4;
-#endif
-}
 
 template <bool NEST>
 __device__ __forceinline__ void optimize(float s, float& w, float& m, float nlr, float mu,
@@ -120,85 +111,158 @@ __device__ __forceinline__ uint32_t wave_index() {
 // The kernel arguments are __restrict__: the schedule and the pointer table
 // are never written by the kernel and W/M never alias the gradients, which
 // lets the compiler fetch descriptors and pointers with scalar loads.
-#define PHUB_KERNEL_ARGS                                                            \
-    const DevSegment* __restrict__ segments, const int64_t* __restrict__ bin_begin, \
-        const float* const* __restrict__ grads, float* __restrict__ weights,        \
-        float* __restrict__ moments, float lr, float mu, float wd, int num_workers, \
-        int64_t resident_elems
+#define PHUB_KERNEL_ARGS                                                                  \
+    const DevTile* __restrict__ tiles, const int32_t* __restrict__ tile_begin,            \
+        const DevRem* __restrict__ rems, const int32_t* __restrict__ rem_begin,           \
+        const float* const* __restrict__ grads, float* __restrict__ weights,              \
+        float* __restrict__ moments, float lr, float mu, float wd, int num_workers
 
-// One segment, exactly NW workers, processed by the calling wave alone.
-template <int NW, int U, bool NEST, bool RES>
-__device__ __forceinline__ void segment_fixed(const float* const* g, float* wb, float* mb,
-                                              uint32_t nvec, float nlr, float mu, float wd) {
-    const uint32_t lane = threadIdx.x & 63u;
-    for (uint32_t base = 0; base < nvec; base += 64u * U) {
-        f4 a[U][NW];
-        f4 wv[U], mv[U];
+// One full tile: kVecPerLane float4 per lane of each array.  g[w], wb and
+// mb are uniform base pointers; the tile starts at float4 index `vec` from
+// them, and lane l takes the float4s at vec + l, + 64, + 128 and + 192.  The
+// per-lane byte offset is formed inside the loop from the tile's (uniform)
+// index, so that the compiler addresses every load and store as uniform
+// base + 32-bit lane offset + immediate.  All NW * kVecPerLane gradient
+// loads and the W and M loads are issued before the first addition.
+template <int NW, bool NEST, bool RES>
+__device__ __forceinline__ void full_tile(const float* const* g, float* wb, float* mb,
+                                          uint32_t vec, float nlr, float mu, float wd) {
+    constexpr int U = kVecPerLane;
+    const uint32_t off = (vec + (threadIdx.x & 63u)) * 16u;
+    f4 a[U][NW];
+    f4 wv[U], mv[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t v = base + u * 64u + lane;
-            if (v < nvec) {
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-                for (int w = 0; w < NW; ++w) a[u][w] = load_stream(g[w], v * 16u);
-            }
-        }
+        for (int w = 0; w < NW; ++w) a[u][w] = load_stream(g[w], off + u * 1024u);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t v = base + u * 64u + lane;
-            if (v < nvec) {
-                wv[u] = load_wm(wb, v * 16u, RES);
-                mv[u] = load_wm(mb, v * 16u, RES);
-            }
-        }
+    for (int u = 0; u < U; ++u) {
+        wv[u] = load_wm(wb, off + u * 1024u, RES);
+        mv[u] = load_wm(mb, off + u * 1024u, RES);
+    }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t v = base + u * 64u + lane;
-            if (v < nvec) {
-                f4 s = a[u][0];
+    for (int u = 0; u < U; ++u) {
+        f4 s = a[u][0];
 #pragma unroll
-                for (int w = 1; w < NW; ++w) s = s + a[u][w];
-                optimize4<NEST>(s, wv[u], mv[u], nlr, mu, wd);
-                store_wm(wb, v * 16u, wv[u], RES);
-                store_wm(mb, v * 16u, mv[u], RES);
-            }
-        }
+        for (int w = 1; w < NW; ++w) s = s + a[u][w];
+        optimize4<NEST>(s, wv[u], mv[u], nlr, mu, wd);
+        store_wm(wb, off + u * 1024u, wv[u], RES);
+        store_wm(mb, off + u * 1024u, mv[u], RES);
     }
 }
 
-// NW > 0: exactly NW workers.
-template <int NW, bool NEST>
-__global__ __launch_bounds__(kBlockThreads) void fused_step_fixed(PHUB_KERNEL_ARGS) {
-    const uint32_t wave = wave_index();
-    const int64_t sb = bin_begin[wave];
-    const int64_t se = bin_begin[wave + 1];
+// The rest of a segment: nvec < 256 float4 then a ragged end of rem < 4
+// elements (one per lane).
+template <int NW, bool NEST, bool RES>
+__device__ __forceinline__ void partial(const float* const* g, float* wb, float* mb,
+                                        uint32_t nvec, uint32_t rem, float nlr, float mu,
+                                        float wd) {
     const uint32_t lane = threadIdx.x & 63u;
+    for (uint32_t v = lane; v < nvec; v += 64u) {
+        f4 a[NW];
+#pragma unroll
+        for (int w = 0; w < NW; ++w) a[w] = load_stream(g[w], v * 16u);
+        f4 wv = load_wm(wb, v * 16u, RES);
+        f4 mv = load_wm(mb, v * 16u, RES);
+        f4 s = a[0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) s = s + a[w];
+        optimize4<NEST>(s, wv, mv, nlr, mu, wd);
+        store_wm(wb, v * 16u, wv, RES);
+        store_wm(mb, v * 16u, mv, RES);
+    }
+    if (lane < rem) {
+        const int64_t i = int64_t(nvec) * 4 + lane;
+        float s = load1(g[0], i);
+#pragma unroll
+        for (int w = 1; w < NW; ++w) s = s + load1(g[w], i);
+        float wv = load1(wb, i), mv = load1(mb, i);
+        optimize<NEST>(s, wv, mv, nlr, mu, wd);
+        store1(wb, i, wv);
+        store1(mb, i, mv);
+    }
+}
+
+// Scalar loads return out of order, so the compiler waits for all of them
+// (lgkmcnt(0)) before it uses any.  `settle` uses values whose loads were
+// issued one tile earlier, so that this single wait happens before the next
+// prefetches are issued; the scheduling barriers keep the compiler from
+// moving the new scalar loads above it (they would then be waited on too).
+__device__ __forceinline__ void settle32(uint32_t v) { asm volatile("" ::"s"(v)); }
+__device__ __forceinline__ void settle64(const void* p) { asm volatile("" ::"s"(p)); }
+
+__device__ __forceinline__ void settle_tile(const DevTile& t) {
+    settle64(reinterpret_cast<const void*>(t.arena_offset));
+    settle32(uint32_t(t.key));
+    settle32(uint32_t(t.vec));
+}
+
+// NW > 0: exactly NW workers.  Each wave first streams its full tiles, with
+// a two-deep prefetch (while tile i streams, the descriptor of tile i + 2
+// and the gradient pointers of tile i + 1 are on their way), then its
+// remainders.
+// Splits a tile's float4 index into a part folded into the base pointers
+// (a multiple of 2^20 float4, 16 MB) and a low part that keeps the per-lane
+// 32-bit byte offset far from overflow.
+constexpr uint32_t kVecLowMask = (1u << 20) - 1;
+
+// One wave per SIMD (one workgroup of 4 waves per CU): the compiler may use
+// the whole register file for loads in flight instead of trading them for
+// occupancy.
+#define PHUB_ONE_WAVE_PER_SIMD __attribute__((amdgpu_waves_per_eu(1, 1)))
+
+template <int NW, bool NEST, bool RES>
+__global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_step_fixed(
+    PHUB_KERNEL_ARGS) {
+    const uint32_t wave = wave_index();
     const float nlr = -lr;
-    for (int64_t si = sb; si < se; ++si) {
-        const DevSegment sg = segments[si];
-        const float* const* kp = grads + int64_t(sg.key) * NW;
+
+    const int32_t tb = tile_begin[wave];
+    const int32_t te = tile_begin[wave + 1];
+    if (tb < te) {
+        const int32_t last = te - 1;
+        DevTile cur = tiles[tb];
+        const float* gc[NW];
+#pragma unroll
+        for (int w = 0; w < NW; ++w) gc[w] = grads[int64_t(cur.key) * NW + w];
+        DevTile nxt = tiles[tb + 1 <= last ? tb + 1 : last];
+        for (int32_t t = tb; t <= last; ++t) {
+            settle_tile(cur);
+            settle_tile(nxt);
+#pragma unroll
+            for (int w = 0; w < NW; ++w) settle64(gc[w]);
+            __builtin_amdgcn_sched_barrier(0);
+            const float* gn[NW];
+#pragma unroll
+            for (int w = 0; w < NW; ++w) gn[w] = grads[int64_t(nxt.key) * NW + w];
+            const DevTile nxt2 = tiles[t + 2 <= last ? t + 2 : last];
+            __builtin_amdgcn_sched_barrier(0);
+
+            const uint32_t vhi = uint32_t(cur.vec) & ~kVecLowMask;
+            const uint32_t vlo = uint32_t(cur.vec) & kVecLowMask;
+            const float* g[NW];
+#pragma unroll
+            for (int w = 0; w < NW; ++w) g[w] = gc[w] + size_t(vhi) * 4;
+            full_tile<NW, NEST, RES>(g, weights + cur.arena_offset - size_t(vlo) * 4,
+                                     moments + cur.arena_offset - size_t(vlo) * 4, vlo, nlr, mu,
+                                     wd);
+            __builtin_amdgcn_sched_barrier(0);
+            cur = nxt;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) gc[w] = gn[w];
+            nxt = nxt2;
+        }
+    }
+
+    const int32_t rb = rem_begin[wave];
+    const int32_t re = rem_begin[wave + 1];
+    for (int32_t r = rb; r < re; ++r) {
+        const DevRem rm = rems[r];
         const float* g[NW];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) g[w] = kp[w] + sg.offset;
-        float* wb = weights + sg.arena_offset;
-        float* mb = moments + sg.arena_offset;
-
-        const uint32_t nvec = uint32_t(sg.count) >> 2;
-        if (sg.arena_offset + sg.count <= resident_elems)
-            segment_fixed<NW, vec_per_lane<NW>(), NEST, true>(g, wb, mb, nvec, nlr, mu, wd);
-        else
-            segment_fixed<NW, vec_per_lane<NW>(), NEST, false>(g, wb, mb, nvec, nlr, mu, wd);
-        // ragged end of a key: fewer than 4 elements, one per lane
-        const uint32_t rem = uint32_t(sg.count) & 3u;
-        if (lane < rem) {
-            const int64_t i = int64_t(nvec) * 4 + lane;
-            float s = load1(g[0], i);
-#pragma unroll
-            for (int w = 1; w < NW; ++w) s = s + load1(g[w], i);
-            float wv = load1(wb, i), mv = load1(mb, i);
-            optimize<NEST>(s, wv, mv, nlr, mu, wd);
-            store1(wb, i, wv);
-            store1(mb, i, mv);
-        }
+        for (int w = 0; w < NW; ++w) g[w] = grads[int64_t(rm.key) * NW + w] + rm.offset;
+        partial<NW, NEST, RES>(g, weights + rm.arena_offset, moments + rm.arena_offset,
+                               uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u, nlr, mu, wd);
     }
 }
 
@@ -206,96 +270,114 @@ __global__ __launch_bounds__(kBlockThreads) void fused_step_fixed(PHUB_KERNEL_AR
 // together, the running sum carried across batches in worker order.
 constexpr int kBatch = 8;
 
-template <bool NEST>
-__global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS) {
-    const uint32_t wave = wave_index();
-    const int64_t sb = bin_begin[wave];
-    const int64_t se = bin_begin[wave + 1];
+template <bool NEST, bool RES>
+__device__ __forceinline__ void run_any(const float* const* kp, int n, int64_t offset, float* wb,
+                                        float* mb, uint32_t nvec, uint32_t rem, float nlr,
+                                        float mu, float wd) {
     const uint32_t lane = threadIdx.x & 63u;
-    const int n = num_workers;
-    const float nlr = -lr;
-    for (int64_t si = sb; si < se; ++si) {
-        const DevSegment sg = segments[si];
-        const float* const* kp = grads + int64_t(sg.key) * n;
-        float* wb = weights + sg.arena_offset;
-        float* mb = moments + sg.arena_offset;
-        const bool res = sg.arena_offset + sg.count <= resident_elems;
-        const uint32_t nvec = uint32_t(sg.count) >> 2;
-        for (uint32_t v = lane; v < nvec; v += 64u) {
-            const uint32_t bo = v * 16u;
-            f4 s = load_stream(kp[0] + sg.offset, bo);
-            for (int w0 = 1; w0 < n; w0 += kBatch) {
-                f4 a[kBatch];
+    for (uint32_t v = lane; v < nvec; v += 64u) {
+        const uint32_t bo = v * 16u;
+        f4 s = load_stream(kp[0] + offset, bo);
+        for (int w0 = 1; w0 < n; w0 += kBatch) {
+            f4 a[kBatch];
 #pragma unroll
-                for (int j = 0; j < kBatch; ++j)
-                    if (w0 + j < n) a[j] = load_stream(kp[w0 + j] + sg.offset, bo);
+            for (int j = 0; j < kBatch; ++j)
+                if (w0 + j < n) a[j] = load_stream(kp[w0 + j] + offset, bo);
 #pragma unroll
-                for (int j = 0; j < kBatch; ++j)
-                    if (w0 + j < n) s = s + a[j];
-            }
-            f4 wv = load_wm(wb, bo, res);
-            f4 mv = load_wm(mb, bo, res);
-            optimize4<NEST>(s, wv, mv, nlr, mu, wd);
-            store_wm(wb, bo, wv, res);
-            store_wm(mb, bo, mv, res);
+            for (int j = 0; j < kBatch; ++j)
+                if (w0 + j < n) s = s + a[j];
         }
-        const uint32_t rem = uint32_t(sg.count) & 3u;
-        if (lane < rem) {
-            const int64_t i = int64_t(nvec) * 4 + lane;
-            float s = load1(kp[0] + sg.offset, i);
-            for (int w = 1; w < n; ++w) s = s + load1(kp[w] + sg.offset, i);
-            float wv = load1(wb, i), mv = load1(mb, i);
-            optimize<NEST>(s, wv, mv, nlr, mu, wd);
-            store1(wb, i, wv);
-            store1(mb, i, mv);
-        }
+        f4 wv = load_wm(wb, bo, RES);
+        f4 mv = load_wm(mb, bo, RES);
+        optimize4<NEST>(s, wv, mv, nlr, mu, wd);
+        store_wm(wb, bo, wv, RES);
+        store_wm(mb, bo, mv, RES);
+    }
+    if (lane < rem) {
+        const int64_t i = int64_t(nvec) * 4 + lane;
+        float s = load1(kp[0] + offset, i);
+        for (int w = 1; w < n; ++w) s = s + load1(kp[w] + offset, i);
+        float wv = load1(wb, i), mv = load1(mb, i);
+        optimize<NEST>(s, wv, mv, nlr, mu, wd);
+        store1(wb, i, wv);
+        store1(mb, i, mv);
     }
 }
 
-#define PHUB_LAUNCH_ARGS                                                                     \
-    p.segments, p.bin_begin, p.grads, p.weights, p.moments, p.lr, p.mu, p.wd, p.num_workers, \
-        p.resident_elems
+template <bool NEST, bool RES>
+__global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS) {
+    const uint32_t wave = wave_index();
+    const int n = num_workers;
+    const float nlr = -lr;
+    const int32_t tb = tile_begin[wave];
+    const int32_t te = tile_begin[wave + 1];
+    for (int32_t t = tb; t < te; ++t) {
+        const DevTile tl = tiles[t];
+        run_any<NEST, RES>(grads + int64_t(tl.key) * n, n, int64_t(tl.vec) * 4,
+                           weights + tl.arena_offset, moments + tl.arena_offset,
+                           uint32_t(kTileElems / 4), 0u, nlr, mu, wd);
+    }
+    const int32_t rb = rem_begin[wave];
+    const int32_t re = rem_begin[wave + 1];
+    for (int32_t r = rb; r < re; ++r) {
+        const DevRem rm = rems[r];
+        run_any<NEST, RES>(grads + int64_t(rm.key) * n, n, rm.offset, weights + rm.arena_offset,
+                           moments + rm.arena_offset, uint32_t(rm.count) >> 2,
+                           uint32_t(rm.count) & 3u, nlr, mu, wd);
+    }
+}
 
-template <int NW>
+#define PHUB_LAUNCH_ARGS                                                                    \
+    p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.weights, p.moments, p.lr, p.mu, \
+        p.wd, p.num_workers
+
+template <int NW, bool RES>
 hipError_t launch_n(const StepParams& p, bool nesterov, int grid, hipStream_t stream) {
     if (nesterov)
-        hipLaunchKernelGGL((fused_step_fixed<NW, true>), dim3(grid), dim3(kBlockThreads), 0, stream,
-                           PHUB_LAUNCH_ARGS);
+        hipLaunchKernelGGL((fused_step_fixed<NW, true, RES>), dim3(grid), dim3(kBlockThreads), 0,
+                           stream, PHUB_LAUNCH_ARGS);
     else
-        hipLaunchKernelGGL((fused_step_fixed<NW, false>), dim3(grid), dim3(kBlockThreads), 0,
+        hipLaunchKernelGGL((fused_step_fixed<NW, false, RES>), dim3(grid), dim3(kBlockThreads), 0,
                            stream, PHUB_LAUNCH_ARGS);
     return hipGetLastError();
 }
 
-}  // namespace
-
-hipError_t launch_fused_step(const StepParams& p, bool nesterov, int grid, hipStream_t stream) {
+template <bool RES>
+hipError_t launch_res(const StepParams& p, bool nesterov, int grid, hipStream_t stream) {
     switch (p.num_workers) {
-        case 1: return launch_n<1>(p, nesterov, grid, stream);
-        case 2: return launch_n<2>(p, nesterov, grid, stream);
-        case 3: return launch_n<3>(p, nesterov, grid, stream);
-        case 4: return launch_n<4>(p, nesterov, grid, stream);
-        case 5: return launch_n<5>(p, nesterov, grid, stream);
-        case 6: return launch_n<6>(p, nesterov, grid, stream);
-        case 7: return launch_n<7>(p, nesterov, grid, stream);
-        case 8: return launch_n<8>(p, nesterov, grid, stream);
-        case 9: return launch_n<9>(p, nesterov, grid, stream);
-        case 10: return launch_n<10>(p, nesterov, grid, stream);
-        case 11: return launch_n<11>(p, nesterov, grid, stream);
-        case 12: return launch_n<12>(p, nesterov, grid, stream);
-        case 13: return launch_n<13>(p, nesterov, grid, stream);
-        case 14: return launch_n<14>(p, nesterov, grid, stream);
-        case 15: return launch_n<15>(p, nesterov, grid, stream);
-        case 16: return launch_n<16>(p, nesterov, grid, stream);
+        case 1: return launch_n<1, RES>(p, nesterov, grid, stream);
+        case 2: return launch_n<2, RES>(p, nesterov, grid, stream);
+        case 3: return launch_n<3, RES>(p, nesterov, grid, stream);
+        case 4: return launch_n<4, RES>(p, nesterov, grid, stream);
+        case 5: return launch_n<5, RES>(p, nesterov, grid, stream);
+        case 6: return launch_n<6, RES>(p, nesterov, grid, stream);
+        case 7: return launch_n<7, RES>(p, nesterov, grid, stream);
+        case 8: return launch_n<8, RES>(p, nesterov, grid, stream);
+        case 9: return launch_n<9, RES>(p, nesterov, grid, stream);
+        case 10: return launch_n<10, RES>(p, nesterov, grid, stream);
+        case 11: return launch_n<11, RES>(p, nesterov, grid, stream);
+        case 12: return launch_n<12, RES>(p, nesterov, grid, stream);
+        case 13: return launch_n<13, RES>(p, nesterov, grid, stream);
+        case 14: return launch_n<14, RES>(p, nesterov, grid, stream);
+        case 15: return launch_n<15, RES>(p, nesterov, grid, stream);
+        case 16: return launch_n<16, RES>(p, nesterov, grid, stream);
         default:
             if (nesterov)
-                hipLaunchKernelGGL((fused_step_any<true>), dim3(grid), dim3(kBlockThreads), 0,
+                hipLaunchKernelGGL((fused_step_any<true, RES>), dim3(grid), dim3(kBlockThreads), 0,
                                    stream, PHUB_LAUNCH_ARGS);
             else
-                hipLaunchKernelGGL((fused_step_any<false>), dim3(grid), dim3(kBlockThreads), 0,
+                hipLaunchKernelGGL((fused_step_any<false, RES>), dim3(grid), dim3(kBlockThreads), 0,
                                    stream, PHUB_LAUNCH_ARGS);
             return hipGetLastError();
     }
+}
+
+}  // namespace
+
+hipError_t launch_fused_step(const StepParams& p, bool nesterov, bool resident, int grid,
+                             hipStream_t stream) {
+    return resident ? launch_res<true>(p, nesterov, grid, stream)
+                    : launch_res<false>(p, nesterov, grid, stream);
 }
 
 }  // namespace phub

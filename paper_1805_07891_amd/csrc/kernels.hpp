@@ -17,20 +17,37 @@ constexpr int kBlockThreads = PHUB_BLOCK_THREADS;
 static_assert(kBlockThreads >= 64 && kBlockThreads <= 1024 && kBlockThreads % 64 == 0,
               "block size must be a multiple of the wave size");
 
-// One scheduled segment as the kernel reads it (32 bytes).
-struct DevSegment {
-    int64_t arena_offset;  // first element's index in the W and M arenas
-    int64_t offset;        // first element's index within the key
+// A tile is what one wave moves per iteration of its hot loop: 4 float4 per
+// lane of each array, i.e. 1024 elements (4 KB) of every gradient, of W and
+// of M.
+constexpr int kVecPerLane = 4;
+constexpr int64_t kTileElems = 64 * 4 * kVecPerLane;
+
+// One full tile (16 bytes): kTileElems elements of a key starting at
+// element 4 * vec.
+struct DevTile {
+    int64_t arena_offset;  // index of the tile's first element in the W and M arenas
     int32_t key;
-    int32_t count;         // elements, >= 1
+    int32_t vec;           // index of the tile's first float4 within the key
+};
+static_assert(sizeof(DevTile) == 16, "DevTile layout");
+
+// The rest of a segment after its full tiles (32 bytes): fewer than
+// kTileElems elements, possibly with a ragged end of up to 3 elements.
+struct DevRem {
+    int64_t arena_offset;  // index of the first element in the W and M arenas
+    int64_t offset;        // index of the first element within the key (multiple of 4)
+    int32_t key;
+    int32_t count;         // elements, 1 .. kTileElems - 1
     int64_t pad;
 };
-static_assert(sizeof(DevSegment) == 32, "DevSegment layout");
+static_assert(sizeof(DevRem) == 32, "DevRem layout");
 
 struct StepParams {
-    const DevSegment* segments;   // grouped by bin (one bin per wave)
-    const int64_t* bin_begin;     // wave w owns [bin_begin[w], bin_begin[w+1]); one entry per
-                                  // wave of the grid, plus one
+    const DevTile* tiles;         // grouped by bin (one bin per wave)
+    const int32_t* tile_begin;    // wave w owns tiles [tile_begin[w], tile_begin[w+1])
+    const DevRem* rems;           // grouped by bin
+    const int32_t* rem_begin;     // wave w owns rems [rem_begin[w], rem_begin[w+1])
     const float* const* grads;    // [key * num_workers + worker], 16-byte aligned
     float* weights;               // W arena
     float* moments;               // M arena
@@ -38,11 +55,13 @@ struct StepParams {
     float mu;
     float wd;
     int num_workers;
-    int64_t resident_elems;  // W/M elements [0, resident_elems) use cache-allocating accesses
 };
 
 // Enqueues one fused aggregate + optimize pass over the whole schedule:
-// `grid` workgroups of kBlockThreads threads.
-hipError_t launch_fused_step(const StepParams& p, bool nesterov, int grid, hipStream_t stream);
+// `grid` workgroups of kBlockThreads threads, one bin per wave (the bin
+// tables have grid * kBlockThreads / 64 + 1 entries).  `resident`: W and M
+// use the cache-allocating policy instead of non-temporal accesses.
+hipError_t launch_fused_step(const StepParams& p, bool nesterov, bool resident, int grid,
+                             hipStream_t stream);
 
 }  // namespace phub

@@ -10,6 +10,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -28,9 +29,9 @@
 #ifndef PHUB_GROUPS_PER_CU
 #define PHUB_GROUPS_PER_CU 1
 #endif
-// Default bytes of W plus M (from the start of the arenas) accessed with the
-// cache-allocating policy so that they can stay in the memory-side cache
-// between steps; the rest streams non-temporally.
+// Default cache budget: a job whose W plus M fit in it reads and writes them
+// with the cache-allocating policy so that they can stay in the memory-side
+// cache between steps; otherwise they stream non-temporally.
 #ifndef PHUB_RESIDENT_BYTES
 #define PHUB_RESIDENT_BYTES 0
 #endif
@@ -81,12 +82,16 @@ struct phub_job {
     int groups = 0;  // workgroups of one launch
     int bins = 0;    // waves with a segment list (groups * waves per workgroup)
     int64_t num_segments = 0;
-    int64_t resident_elems = 0;
+    int64_t num_tiles = 0;
+    int64_t num_rems = 0;
+    bool resident = false;  // W and M stay in the memory-side cache between steps
 
     float* weights = nullptr;
     float* moments = nullptr;
-    phub::DevSegment* d_segments = nullptr;
-    int64_t* d_bin_begin = nullptr;
+    phub::DevTile* d_tiles = nullptr;
+    int32_t* d_tile_begin = nullptr;
+    phub::DevRem* d_rems = nullptr;
+    int32_t* d_rem_begin = nullptr;
     const float** d_grads = nullptr;
 
     std::vector<const float*> grads;  // host table, [key * N + worker]
@@ -127,8 +132,10 @@ bool is_live(const phub_job* j) {
 
 void release(phub_job* j) {
     if (j->d_grads) (void)hipFree(j->d_grads);
-    if (j->d_bin_begin) (void)hipFree(j->d_bin_begin);
-    if (j->d_segments) (void)hipFree(j->d_segments);
+    if (j->d_tile_begin) (void)hipFree(j->d_tile_begin);
+    if (j->d_tiles) (void)hipFree(j->d_tiles);
+    if (j->d_rem_begin) (void)hipFree(j->d_rem_begin);
+    if (j->d_rems) (void)hipFree(j->d_rems);
     if (j->moments) (void)hipFree(j->moments);
     if (j->weights) (void)hipFree(j->weights);
     for (int i = 0; i < kStageSlots; ++i) {
@@ -323,7 +330,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     }
     j->schedule = schedule;
     j->num_segments = int64_t(plan.segments.size());
-    j->resident_elems = resident_bytes / 8;  // W and M, 4 bytes each
+    j->resident = resident_bytes > 0 && 2 * j->arena_elems * int64_t(sizeof(float)) <= resident_bytes;
 
 #define PHUB_TRY(call, what)                 \
     do {                                     \
@@ -352,27 +359,61 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         PHUB_TRY(hipMemsetAsync(j->weights, 0, arena_bytes, j->stream), "hipMemsetAsync(W)");
         PHUB_TRY(hipMemsetAsync(j->moments, 0, arena_bytes, j->stream), "hipMemsetAsync(M)");
 
-        std::vector<phub::DevSegment> dseg(plan.segments.size());
-        for (size_t i = 0; i < plan.segments.size(); ++i) {
-            const phub::PlanSegment& s = plan.segments[i];
-            dseg[i] = {j->arena_offset[s.key] + s.offset, s.offset, s.key, s.count, 0};
+        // Device form of the schedule: each bin's segments become full tiles
+        // (the kernel's straight-line hot loop) and at most one remainder
+        // each (partial tile and ragged end), in segment order.
+        std::vector<phub::DevTile> dtiles;
+        std::vector<phub::DevRem> drems;
+        std::vector<int32_t> tile_begin(1, 0), rem_begin(1, 0);
+        const int nb = int(plan.bin_begin.size()) - 1;
+        for (int b = 0; b < nb; ++b) {
+            for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
+                const phub::PlanSegment& sg = plan.segments[i];
+                const int64_t ao = j->arena_offset[sg.key] + sg.offset;
+                const int64_t nfull = sg.count / phub::kTileElems;
+                for (int64_t t = 0; t < nfull; ++t)
+                    dtiles.push_back({ao + t * phub::kTileElems, sg.key,
+                                      int32_t((sg.offset + t * phub::kTileElems) / 4)});
+                const int64_t done = nfull * phub::kTileElems;
+                if (done < sg.count)
+                    drems.push_back({ao + done, sg.offset + done, sg.key,
+                                     int32_t(sg.count - done), 0});
+            }
+            if (dtiles.size() > size_t(INT32_MAX) || drems.size() > size_t(INT32_MAX)) {
+                rc = fail(PHUB_EINVAL, "schedule too large");
+                goto fail_cleanup;
+            }
+            tile_begin.push_back(int32_t(dtiles.size()));
+            rem_begin.push_back(int32_t(drems.size()));
         }
-        const size_t seg_bytes = std::max<size_t>(dseg.size(), 1) * sizeof(phub::DevSegment);
-        const size_t gb_bytes = plan.bin_begin.size() * sizeof(int64_t);
+        j->num_tiles = int64_t(dtiles.size());
+        j->num_rems = int64_t(drems.size());
+        const size_t tile_bytes = std::max<size_t>(dtiles.size(), 1) * sizeof(phub::DevTile);
+        const size_t rem_bytes = std::max<size_t>(drems.size(), 1) * sizeof(phub::DevRem);
+        const size_t tb_bytes = tile_begin.size() * sizeof(int32_t);
+        const size_t rb_bytes = rem_begin.size() * sizeof(int32_t);
         const size_t tab_bytes = j->grads.size() * sizeof(const float*);
-        if (hipMalloc(&j->d_segments, seg_bytes) != hipSuccess ||
-            hipMalloc(&j->d_bin_begin, gb_bytes) != hipSuccess ||
+        if (hipMalloc(&j->d_tiles, tile_bytes) != hipSuccess ||
+            hipMalloc(&j->d_tile_begin, tb_bytes) != hipSuccess ||
+            hipMalloc(&j->d_rems, rem_bytes) != hipSuccess ||
+            hipMalloc(&j->d_rem_begin, rb_bytes) != hipSuccess ||
             hipMalloc(&j->d_grads, tab_bytes) != hipSuccess) {
             (void)hipGetLastError();
             rc = fail(PHUB_ENOMEM, "device allocation of the schedule failed");
             goto fail_cleanup;
         }
-        if (!dseg.empty())
-            PHUB_TRY(hipMemcpy(j->d_segments, dseg.data(), dseg.size() * sizeof(phub::DevSegment),
+        if (!dtiles.empty())
+            PHUB_TRY(hipMemcpy(j->d_tiles, dtiles.data(), dtiles.size() * sizeof(phub::DevTile),
                                hipMemcpyHostToDevice),
-                     "hipMemcpy(schedule)");
-        PHUB_TRY(hipMemcpy(j->d_bin_begin, plan.bin_begin.data(), gb_bytes, hipMemcpyHostToDevice),
-                 "hipMemcpy(bin table)");
+                     "hipMemcpy(tiles)");
+        if (!drems.empty())
+            PHUB_TRY(hipMemcpy(j->d_rems, drems.data(), drems.size() * sizeof(phub::DevRem),
+                               hipMemcpyHostToDevice),
+                     "hipMemcpy(remainders)");
+        PHUB_TRY(hipMemcpy(j->d_tile_begin, tile_begin.data(), tb_bytes, hipMemcpyHostToDevice),
+                 "hipMemcpy(tile bins)");
+        PHUB_TRY(hipMemcpy(j->d_rem_begin, rem_begin.data(), rb_bytes, hipMemcpyHostToDevice),
+                 "hipMemcpy(remainder bins)");
         for (int i = 0; i < kStageSlots; ++i) {
             if (hipHostMalloc(reinterpret_cast<void**>(&j->stage[i]), tab_bytes,
                               hipHostMallocDefault) != hipSuccess) {
@@ -453,8 +494,10 @@ int phub_step(phub_job* j) {
         if (int rc = upload_table(j)) return rc;
     if (j->groups > 0) {
         phub::StepParams p;
-        p.segments = j->d_segments;
-        p.bin_begin = j->d_bin_begin;
+        p.tiles = j->d_tiles;
+        p.tile_begin = j->d_tile_begin;
+        p.rems = j->d_rems;
+        p.rem_begin = j->d_rem_begin;
         p.grads = j->d_grads;
         p.weights = j->weights;
         p.moments = j->moments;
@@ -462,8 +505,7 @@ int phub_step(phub_job* j) {
         p.mu = j->mu;
         p.wd = j->wd;
         p.num_workers = j->num_workers;
-        p.resident_elems = j->resident_elems;
-        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->groups, j->stream);
+        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->resident, j->groups, j->stream);
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
     }
     std::fill(j->pushed.begin(), j->pushed.end(), 0);
