@@ -112,6 +112,9 @@ def main(argv=None) -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of the CPU oracle baseline (0 skips it)")
+    ap.add_argument("--resident-bytes", type=int, default=None,
+                    help="per-job budget for keeping W and M in the memory-side cache "
+                         "(library default if omitted)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 512 MiB device copy three times (a known-size "
                          "reference for hardware byte counters)")
@@ -145,7 +148,7 @@ def main(argv=None) -> int:
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
         stream = torch.cuda.Stream(device=dev)
-        job = TorchJob(spec, dev, stream=stream, lib=lib)
+        job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
              for w in range(spec.num_workers)]
@@ -189,7 +192,8 @@ def main(argv=None) -> int:
     dom_bytes = wl.jobs[dom].hbm_bytes_per_step()
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
     traffic = measured_traffic(args.workload)
-    groups, threads, segs = jobs[dom].info()
+    groups, threads, segs, _ = jobs[dom].info()
+    cache_resident = [job.info()[3] for job in jobs]
 
     baseline = None
     if args.cpu_seconds > 0:
@@ -211,7 +215,8 @@ def main(argv=None) -> int:
         "config": {
             "workload": args.workload,
             "jobs": [{"name": j.name, "workers": j.num_workers, "keys": j.num_keys,
-                      "params": j.num_params} for j in wl.jobs],
+                      "params": j.num_params, "wm_cache_resident": bool(r)}
+                     for j, r in zip(wl.jobs, cache_resident)],
             "chunk_bytes": wl.jobs[0].chunk_bytes,
             "optimizer": {"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
                           "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov},

@@ -91,20 +91,24 @@ enum phub_schedule {
 /* Optional settings of phub_init_ex. */
 typedef struct phub_options {
     int schedule;           /* a phub_schedule value */
-    int64_t resident_bytes; /* a budget in bytes for keeping W and M in the
-                               GPU's memory-side cache between steps (the
-                               paper's cached model, section 4.5): when the
-                               whole W and M arenas (8 bytes per padded
-                               element) fit in it, they are read and written
-                               with the cache-allocating policy; otherwise, and
-                               for 0, they stream non-temporally like the
-                               gradients.  -1 keeps the default (0).  Results
-                               do not depend on it. */
+    int64_t resident_bytes; /* cache budget in bytes for this job's W and M
+                               (the paper's cached model, section 4.5): when
+                               W plus M (8 bytes per padded element) fit in
+                               it, they are read and written with the
+                               cache-allocating policy so that they can stay
+                               in the GPU's memory-side cache between steps;
+                               otherwise, and for 0, they stream
+                               non-temporally like the gradients.  -1: the
+                               default, a per-device budget of 256 MiB (the
+                               memory-side cache of MI355X) shared first come,
+                               first served by the live jobs created with -1
+                               and given back by phub_destroy.  Results do
+                               not depend on it. */
 } phub_options;
 
 /*
  * phub_init_ex - phub_init with options (NULL means the defaults: LPT
- * schedule, no resident bytes).  Errors as phub_init, plus PHUB_EINVAL for
+ * schedule, shared cache budget).  Errors as phub_init, plus PHUB_EINVAL for
  * an unknown schedule or resident_bytes < -1.
  */
 int phub_init_ex(phub_job **out, int num_workers, int num_keys, const int64_t *key_elems,
@@ -182,10 +186,13 @@ int phub_get_stream(phub_job *job, void **hip_stream);
 
 /*
  * phub_job_info - launch shape of the job's step: the number of workgroups
- * of one launch (0 if every key is empty), the threads per workgroup and the
- * number of work segments in the schedule.  Any output may be NULL.
+ * of one launch (0 if every key is empty), the threads per workgroup, the
+ * number of work segments in the schedule, and 1 if W and M use the
+ * cache-allocating policy (0 if they stream non-temporally).  Any output
+ * may be NULL.
  */
-int phub_job_info(phub_job *job, int *workgroups, int *threads_per_group, int64_t *segments);
+int phub_job_info(phub_job *job, int *workgroups, int *threads_per_group, int64_t *segments,
+                  int *cache_resident);
 
 /*
  * phub_destroy - wait for the job's work, free its memory (W, M, schedule,

@@ -39,6 +39,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <utility>
 
 #include "kernels.hpp"
 
@@ -83,14 +84,23 @@ __device__ __forceinline__ f4 load_stream(const float* base, uint32_t byte_off) 
     return __builtin_nontemporal_load((const PHUB_GLOBAL f4*)(b + byte_off));
 }
 
-__device__ __forceinline__ f4 load_wm(const float* base, uint32_t byte_off, bool resident) {
+// W and M accesses.  The policy is a template argument resolved with
+// `if constexpr`: written as a run-time choice between two loads of the same
+// address, the compiler merges the two loads into one and drops the
+// non-temporal hint.
+template <bool RES>
+__device__ __forceinline__ f4 load_wm(const float* base, uint32_t byte_off) {
     const PHUB_GLOBAL f4* a = (const PHUB_GLOBAL f4*)((const PHUB_GLOBAL char*)base + byte_off);
-    return resident ? *a : __builtin_nontemporal_load(a);
+    if constexpr (RES)
+        return *a;
+    else
+        return __builtin_nontemporal_load(a);
 }
 
-__device__ __forceinline__ void store_wm(float* base, uint32_t byte_off, const f4& v, bool resident) {
+template <bool RES>
+__device__ __forceinline__ void store_wm(float* base, uint32_t byte_off, const f4& v) {
     PHUB_GLOBAL f4* a = (PHUB_GLOBAL f4*)((PHUB_GLOBAL char*)base + byte_off);
-    if (resident)
+    if constexpr (RES)
         *a = v;
     else
         __builtin_nontemporal_store(v, a);
@@ -117,38 +127,177 @@ __device__ __forceinline__ uint32_t wave_index() {
         const float* const* __restrict__ grads, float* __restrict__ weights,              \
         float* __restrict__ moments, float lr, float mu, float wd, int num_workers
 
-// One full tile: kVecPerLane float4 per lane of each array.  g[w], wb and
-// mb are uniform base pointers; the tile starts at float4 index `vec` from
-// them, and lane l takes the float4s at vec + l, + 64, + 128 and + 192.  The
-// per-lane byte offset is formed inside the loop from the tile's (uniform)
-// index, so that the compiler addresses every load and store as uniform
-// base + 32-bit lane offset + immediate.  All NW * kVecPerLane gradient
-// loads and the W and M loads are issued before the first addition.
-template <int NW, bool NEST, bool RES>
-__device__ __forceinline__ void full_tile(const float* const* g, float* wb, float* mb,
-                                          uint32_t vec, float nlr, float mu, float wd) {
-    constexpr int U = kVecPerLane;
-    const uint32_t off = (vec + (threadIdx.x & 63u)) * 16u;
-    f4 a[U][NW];
-    f4 wv[U], mv[U];
+// Splits a tile's float4 index into a part folded into the base pointers
+// (a multiple of 2^20 float4, 16 MB) and a low part that keeps the per-lane
+// 32-bit byte offset far from overflow.
+constexpr uint32_t kVecLowMask = (1u << 20) - 1;
+
+// The streams of one full tile: uniform base pointers of the NW gradients,
+// of W and of M, and the lane's byte offset of its first float4 from them.
+// Lane l takes the float4s at tile float4 index l, l + 64, l + 128 and
+// l + 192 (kVecPerLane pieces of 1 KB per wave), so every access is a
+// uniform base in SGPRs + 32-bit lane offset + immediate.
+template <int NW>
+struct TileStreams {
+    const float* g[NW];
+    float* w;
+    float* m;
+    uint32_t off;
+};
+
+template <int NW>
+__device__ __forceinline__ void tile_bases(TileStreams<NW>& s, const DevTile& d, float* weights,
+                                           float* moments) {
+    const uint32_t vlo = uint32_t(d.vec) & kVecLowMask;
+    s.w = weights + d.arena_offset - size_t(vlo) * 4;
+    s.m = moments + d.arena_offset - size_t(vlo) * 4;
+    s.off = (vlo + (threadIdx.x & 63u)) * 16u;
+}
+
+// Streams of a tile from its key's pointer row in memory (scalar loads).
+template <int NW>
+__device__ __forceinline__ void tile_streams(TileStreams<NW>& s, const DevTile& d,
+                                             const float* const* row, float* weights,
+                                             float* moments) {
+    const uint32_t vhi = uint32_t(d.vec) & ~kVecLowMask;
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int w = 0; w < NW; ++w) s.g[w] = row[w] + size_t(vhi) * 4;
+    tile_bases<NW>(s, d, weights, moments);
+}
+
+// A key's pointer row fetched with one vector load, lane w holding worker
+// w's pointer (lanes past the row repeat its last entry).  Held this way
+// the next tile's row costs two VGPRs instead of 2 * NW SGPRs, which
+// matters while the current tile's pointers still occupy SGPRs.
+template <int NW>
+__device__ __forceinline__ uint64_t load_row(const float* const* row) {
+    const uint32_t l = threadIdx.x & 63u;
+    const uint32_t i = l < uint32_t(NW) ? l : uint32_t(NW - 1);
+    return ((const PHUB_GLOBAL uint64_t*)row)[i];
+}
+
+__device__ __forceinline__ const float* lane_pointer(uint64_t row, int w) {
+    const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(row)), w));
+    const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(row >> 32)), w));
+    return reinterpret_cast<const float*>((uint64_t(hi) << 32) | lo);
+}
+
+// Streams of a tile from a pointer row held one per lane.
+template <int NW>
+__device__ __forceinline__ void tile_streams(TileStreams<NW>& s, const DevTile& d, uint64_t row,
+                                             float* weights, float* moments) {
+    const uint32_t vhi = uint32_t(d.vec) & ~kVecLowMask;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) a[u][w] = load_stream(g[w], off + u * 1024u);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        wv[u] = load_wm(wb, off + u * 1024u, RES);
-        mv[u] = load_wm(mb, off + u * 1024u, RES);
+    for (int w = 0; w < NW; ++w) s.g[w] = lane_pointer(row, w) + size_t(vhi) * 4;
+    tile_bases<NW>(s, d, weights, moments);
+}
+
+// Issue order of a tile's loads: for each of the kVecPerLane pieces, W, M,
+// then the gradients in worker order; kTileLoads loads per tile.  A wave
+// keeps a window of loads in flight beyond the one it waits for, and the
+// window runs on into the wave's next tile.  Its depth follows the W/M
+// policy (measured on MI355X):
+//  - non-temporal W and M: a shallow window (kShallowAhead loads, a few KB
+//    per wave) with the W and M reads and writes spread through the tile
+//    moves more bytes than a deep one; deep windows flood the memory system
+//    with open streams;
+//  - W and M held in the memory-side cache: a whole tile ahead (every load
+//    of the next tile in flight while this one is consumed), since only the
+//    gradient streams then reach HBM.
+#ifndef PHUB_LOADS_AHEAD
+#define PHUB_LOADS_AHEAD 3
+#endif
+constexpr int kShallowAhead = PHUB_LOADS_AHEAD;
+
+template <int NW>
+constexpr int kTileLoads = kVecPerLane * (NW + 2);
+
+template <int NW, bool RES>
+constexpr int kAhead = RES ? kTileLoads<NW> - 1 : kShallowAhead;
+
+template <int NW, bool RES>
+constexpr int kRing = kAhead<NW, RES> + 1;
+
+template <int NW, bool RES, int I>
+__device__ __forceinline__ f4 tile_load(const TileStreams<NW>& s) {
+    constexpr int k = I % (NW + 2);
+    constexpr uint32_t o = uint32_t(I / (NW + 2)) * 1024u;
+    if constexpr (k == 0)
+        return load_wm<RES>(s.w, s.off + o);
+    else if constexpr (k == 1)
+        return load_wm<RES>(s.m, s.off + o);
+    else
+        return load_stream(s.g[k - 2], s.off + o);
+}
+
+template <int NW, bool RES>
+struct TilePipe {
+    static constexpr int R = kRing<NW, RES>;
+    f4 ring[R];            // loads in flight, load j of a tile in slot j % R
+    f4 acc[kVecPerLane];   // running gradient sums
+    f4 wv[kVecPerLane];
+    f4 mv[kVecPerLane];
+};
+
+// Step I of a tile: issue load I + kAhead (of this tile, or of the
+// next one if there is one), then consume load I.  After the last gradient
+// of a piece, that piece is optimized and written back.  Just before the
+// first load of the next tile is issued, the next tile's streams are formed
+// from its descriptor and pointer row, which were fetched at the start of
+// this tile.
+template <int NW, bool NEST, bool RES, int I>
+__device__ __forceinline__ void tile_step(TilePipe<NW, RES>& p, const TileStreams<NW>& a,
+                                          TileStreams<NW>& b, const DevTile& nd,
+                                          uint64_t nrow, bool has_next,
+                                          float* weights, float* moments, float nlr, float mu,
+                                          float wd) {
+    constexpr int L = kTileLoads<NW>;
+    constexpr int R = kRing<NW, RES>;
+    constexpr int J = I + kAhead<NW, RES>;
+    if constexpr (J < L) {
+        p.ring[J % R] = tile_load<NW, RES, J>(a);
+    } else {
+        if constexpr (J == L) tile_streams<NW>(b, nd, nrow, weights, moments);
+        if (has_next) p.ring[J % R] = tile_load<NW, RES, J - L>(b);
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        f4 s = a[u][0];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) s = s + a[u][w];
-        optimize4<NEST>(s, wv[u], mv[u], nlr, mu, wd);
-        store_wm(wb, off + u * 1024u, wv[u], RES);
-        store_wm(mb, off + u * 1024u, mv[u], RES);
+    __builtin_amdgcn_sched_barrier(0);
+    const f4 v = p.ring[I % R];
+    constexpr int k = I % (NW + 2);
+    constexpr int u = I / (NW + 2);
+    if constexpr (k == 0)
+        p.wv[u] = v;
+    else if constexpr (k == 1)
+        p.mv[u] = v;
+    else if constexpr (k == 2)
+        p.acc[u] = v;
+    else
+        p.acc[u] = p.acc[u] + v;
+    // Keep the addition (and so the wait for load I) at this step: the
+    // compiler would otherwise sink the additions of the last piece past the
+    // next-tile branch to their use, and issue that piece's loads as a burst.
+    if constexpr (k >= 3) asm volatile("" : "+v"(p.acc[u]));
+    if constexpr (k == NW + 1) {
+        optimize4<NEST>(p.acc[u], p.wv[u], p.mv[u], nlr, mu, wd);
+        store_wm<RES>(a.w, a.off + u * 1024u, p.wv[u]);
+        store_wm<RES>(a.m, a.off + u * 1024u, p.mv[u]);
     }
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int NW, bool NEST, bool RES, int... I>
+__device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>, TilePipe<NW, RES>& p,
+                                           const TileStreams<NW>& a, TileStreams<NW>& b,
+                                           const DevTile& nd, uint64_t nrow,
+                                           bool has_next, float* weights, float* moments,
+                                           float nlr, float mu, float wd) {
+    (tile_step<NW, NEST, RES, I>(p, a, b, nd, nrow, has_next, weights, moments, nlr, mu, wd),
+     ...);
+}
+
+template <int NW, bool RES, int... I>
+__device__ __forceinline__ void tile_prologue(std::integer_sequence<int, I...>, TilePipe<NW, RES>& p,
+                                              const TileStreams<NW>& a) {
+    ((p.ring[I % kRing<NW, RES>] = tile_load<NW, RES, I>(a)), ...);
 }
 
 // The rest of a segment: nvec < 256 float4 then a ragged end of rem < 4
@@ -162,14 +311,14 @@ __device__ __forceinline__ void partial(const float* const* g, float* wb, float*
         f4 a[NW];
 #pragma unroll
         for (int w = 0; w < NW; ++w) a[w] = load_stream(g[w], v * 16u);
-        f4 wv = load_wm(wb, v * 16u, RES);
-        f4 mv = load_wm(mb, v * 16u, RES);
+        f4 wv = load_wm<RES>(wb, v * 16u);
+        f4 mv = load_wm<RES>(mb, v * 16u);
         f4 s = a[0];
 #pragma unroll
         for (int w = 1; w < NW; ++w) s = s + a[w];
         optimize4<NEST>(s, wv, mv, nlr, mu, wd);
-        store_wm(wb, v * 16u, wv, RES);
-        store_wm(mb, v * 16u, mv, RES);
+        store_wm<RES>(wb, v * 16u, wv);
+        store_wm<RES>(mb, v * 16u, mv);
     }
     if (lane < rem) {
         const int64_t i = int64_t(nvec) * 4 + lane;
@@ -183,37 +332,20 @@ __device__ __forceinline__ void partial(const float* const* g, float* wb, float*
     }
 }
 
-// Scalar loads return out of order, so the compiler waits for all of them
-// (lgkmcnt(0)) before it uses any.  `settle` uses values whose loads were
-// issued one tile earlier, so that this single wait happens before the next
-// prefetches are issued; the scheduling barriers keep the compiler from
-// moving the new scalar loads above it (they would then be waited on too).
-__device__ __forceinline__ void settle32(uint32_t v) { asm volatile("" ::"s"(v)); }
-__device__ __forceinline__ void settle64(const void* p) { asm volatile("" ::"s"(p)); }
-
-__device__ __forceinline__ void settle_tile(const DevTile& t) {
-    settle64(reinterpret_cast<const void*>(t.arena_offset));
-    settle32(uint32_t(t.key));
-    settle32(uint32_t(t.vec));
-}
-
-// NW > 0: exactly NW workers.  Each wave first streams its full tiles, with
-// a two-deep prefetch (while tile i streams, the descriptor of tile i + 2
-// and the gradient pointers of tile i + 1 are on their way), then its
-// remainders.
-// Splits a tile's float4 index into a part folded into the base pointers
-// (a multiple of 2^20 float4, 16 MB) and a low part that keeps the per-lane
-// 32-bit byte offset far from overflow.
-constexpr uint32_t kVecLowMask = (1u << 20) - 1;
-
-// One wave per SIMD (one workgroup of 4 waves per CU): the compiler may use
-// the whole register file for loads in flight instead of trading them for
-// occupancy.
+// NW > 0: exactly NW workers.  Each wave first streams its full tiles
+// through the load window, then its remainders.  At the start of tile t the
+// wave fetches the pointer row of tile t + 1 (one vector load), whose
+// descriptor it fetched at the start of tile t - 1, and the descriptor of
+// tile t + 2 (a scalar load); both have long arrived when the window
+// reaches tile t + 1.
+//
+// One wave per SIMD (one workgroup of 4 waves per CU).
 #define PHUB_ONE_WAVE_PER_SIMD __attribute__((amdgpu_waves_per_eu(1, 1)))
 
 template <int NW, bool NEST, bool RES>
 __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_step_fixed(
     PHUB_KERNEL_ARGS) {
+    static_assert(kTileLoads<NW> % kRing<NW, RES> == 0, "the load window must wrap with the tile");
     const uint32_t wave = wave_index();
     const float nlr = -lr;
 
@@ -221,36 +353,23 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
     const int32_t te = tile_begin[wave + 1];
     if (tb < te) {
         const int32_t last = te - 1;
-        DevTile cur = tiles[tb];
-        const float* gc[NW];
-#pragma unroll
-        for (int w = 0; w < NW; ++w) gc[w] = grads[int64_t(cur.key) * NW + w];
-        DevTile nxt = tiles[tb + 1 <= last ? tb + 1 : last];
-        for (int32_t t = tb; t <= last; ++t) {
-            settle_tile(cur);
-            settle_tile(nxt);
-#pragma unroll
-            for (int w = 0; w < NW; ++w) settle64(gc[w]);
-            __builtin_amdgcn_sched_barrier(0);
-            const float* gn[NW];
-#pragma unroll
-            for (int w = 0; w < NW; ++w) gn[w] = grads[int64_t(nxt.key) * NW + w];
-            const DevTile nxt2 = tiles[t + 2 <= last ? t + 2 : last];
-            __builtin_amdgcn_sched_barrier(0);
-
-            const uint32_t vhi = uint32_t(cur.vec) & ~kVecLowMask;
-            const uint32_t vlo = uint32_t(cur.vec) & kVecLowMask;
-            const float* g[NW];
-#pragma unroll
-            for (int w = 0; w < NW; ++w) g[w] = gc[w] + size_t(vhi) * 4;
-            full_tile<NW, NEST, RES>(g, weights + cur.arena_offset - size_t(vlo) * 4,
-                                     moments + cur.arena_offset - size_t(vlo) * 4, vlo, nlr, mu,
-                                     wd);
-            __builtin_amdgcn_sched_barrier(0);
-            cur = nxt;
-#pragma unroll
-            for (int w = 0; w < NW; ++w) gc[w] = gn[w];
-            nxt = nxt2;
+        TilePipe<NW, RES> p;
+        TileStreams<NW> a, b;
+        {
+            const DevTile first = tiles[tb];
+            tile_streams<NW>(a, first, grads + int64_t(first.key) * NW, weights, moments);
+        }
+        DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
+        tile_prologue<NW, RES>(std::make_integer_sequence<int, kAhead<NW, RES>>{}, p, a);
+        for (int32_t t = tb;; ++t) {
+            const bool has_next = t < last;
+            const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
+            const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
+            tile_steps<NW, NEST, RES>(std::make_integer_sequence<int, kTileLoads<NW>>{}, p, a, b,
+                                      nd, nrow, has_next, weights, moments, nlr, mu, wd);
+            if (!has_next) break;
+            a = b;
+            nd = nd2;
         }
     }
 
@@ -287,11 +406,11 @@ __device__ __forceinline__ void run_any(const float* const* kp, int n, int64_t o
             for (int j = 0; j < kBatch; ++j)
                 if (w0 + j < n) s = s + a[j];
         }
-        f4 wv = load_wm(wb, bo, RES);
-        f4 mv = load_wm(mb, bo, RES);
+        f4 wv = load_wm<RES>(wb, bo);
+        f4 mv = load_wm<RES>(mb, bo);
         optimize4<NEST>(s, wv, mv, nlr, mu, wd);
-        store_wm(wb, bo, wv, RES);
-        store_wm(mb, bo, mv, RES);
+        store_wm<RES>(wb, bo, wv);
+        store_wm<RES>(mb, bo, mv);
     }
     if (lane < rem) {
         const int64_t i = int64_t(nvec) * 4 + lane;
@@ -333,12 +452,21 @@ __global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS
 
 template <int NW, bool RES>
 hipError_t launch_n(const StepParams& p, bool nesterov, int grid, hipStream_t stream) {
-    if (nesterov)
-        hipLaunchKernelGGL((fused_step_fixed<NW, true, RES>), dim3(grid), dim3(kBlockThreads), 0,
-                           stream, PHUB_LAUNCH_ARGS);
-    else
-        hipLaunchKernelGGL((fused_step_fixed<NW, false, RES>), dim3(grid), dim3(kBlockThreads), 0,
-                           stream, PHUB_LAUNCH_ARGS);
+    if constexpr (kTileLoads<NW> % kRing<NW, RES> == 0) {
+        if (nesterov)
+            hipLaunchKernelGGL((fused_step_fixed<NW, true, RES>), dim3(grid), dim3(kBlockThreads),
+                               0, stream, PHUB_LAUNCH_ARGS);
+        else
+            hipLaunchKernelGGL((fused_step_fixed<NW, false, RES>), dim3(grid),
+                               dim3(kBlockThreads), 0, stream, PHUB_LAUNCH_ARGS);
+    } else {
+        if (nesterov)
+            hipLaunchKernelGGL((fused_step_any<true, RES>), dim3(grid), dim3(kBlockThreads), 0,
+                               stream, PHUB_LAUNCH_ARGS);
+        else
+            hipLaunchKernelGGL((fused_step_any<false, RES>), dim3(grid), dim3(kBlockThreads), 0,
+                               stream, PHUB_LAUNCH_ARGS);
+    }
     return hipGetLastError();
 }
 

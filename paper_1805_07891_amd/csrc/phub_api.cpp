@@ -18,6 +18,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <unordered_set>
 #include <vector>
 
@@ -29,11 +30,14 @@
 #ifndef PHUB_GROUPS_PER_CU
 #define PHUB_GROUPS_PER_CU 1
 #endif
-// Default cache budget: a job whose W plus M fit in it reads and writes them
-// with the cache-allocating policy so that they can stay in the memory-side
-// cache between steps; otherwise they stream non-temporally.
-#ifndef PHUB_RESIDENT_BYTES
-#define PHUB_RESIDENT_BYTES 0
+// Default cache budget per device, shared by the jobs created with the
+// default option: the size of MI355X's memory-side cache (256 MiB).  A job
+// whose W plus M fit in what is left of it reads and writes them with the
+// cache-allocating policy, so that they can stay in that cache between
+// steps (the paper's cached model, section 4.5); otherwise they stream
+// non-temporally like the gradients.
+#ifndef PHUB_DEVICE_CACHE_BYTES
+#define PHUB_DEVICE_CACHE_BYTES (int64_t(256) << 20)
 #endif
 // The LPT schedule refines chunks until there are this many items per bin.
 constexpr int kLptItemsPerBin = 32;
@@ -61,6 +65,8 @@ int hip_fail(hipError_t e, const char* what) {
 
 std::mutex g_live_mu;
 std::unordered_set<const void*> g_live;
+// Bytes of the default cache budget held by live jobs, per device (under g_live_mu).
+std::unordered_map<int, int64_t> g_cache_claimed;
 
 }  // namespace
 
@@ -85,6 +91,7 @@ struct phub_job {
     int64_t num_tiles = 0;
     int64_t num_rems = 0;
     bool resident = false;  // W and M stay in the memory-side cache between steps
+    int64_t cache_claim = 0;  // bytes of the device's default cache budget this job holds
 
     float* weights = nullptr;
     float* moments = nullptr;
@@ -259,7 +266,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
         return fail(PHUB_EINVAL, "lr, momentum and weight_decay must be finite");
     int schedule = phub::kScheduleLpt;
-    int64_t resident_bytes = PHUB_RESIDENT_BYTES;
+    int64_t resident_bytes = -1;  // -1: the shared per-device budget
     if (options) {
         if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
@@ -330,7 +337,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     }
     j->schedule = schedule;
     j->num_segments = int64_t(plan.segments.size());
-    j->resident = resident_bytes > 0 && 2 * j->arena_elems * int64_t(sizeof(float)) <= resident_bytes;
+    const int64_t wm_bytes = 2 * j->arena_elems * int64_t(sizeof(float));
+    if (resident_bytes >= 0) j->resident = wm_bytes > 0 && wm_bytes <= resident_bytes;
 
 #define PHUB_TRY(call, what)                 \
     do {                                     \
@@ -430,6 +438,14 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
 
     {
         std::lock_guard<std::mutex> lk(g_live_mu);
+        if (resident_bytes < 0 && wm_bytes > 0) {
+            int64_t& claimed = g_cache_claimed[j->device];
+            if (claimed + wm_bytes <= PHUB_DEVICE_CACHE_BYTES) {
+                claimed += wm_bytes;
+                j->cache_claim = wm_bytes;
+                j->resident = true;
+            }
+        }
         g_live.insert(j);
     }
     *out = j;
@@ -545,11 +561,13 @@ int phub_get_stream(phub_job* j, void** hip_stream) {
     return PHUB_OK;
 }
 
-int phub_job_info(phub_job* j, int* workgroups, int* threads_per_group, int64_t* segments) {
+int phub_job_info(phub_job* j, int* workgroups, int* threads_per_group, int64_t* segments,
+                  int* cache_resident) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     if (workgroups) *workgroups = j->groups;
     if (threads_per_group) *threads_per_group = phub::kBlockThreads;
     if (segments) *segments = j->num_segments;
+    if (cache_resident) *cache_resident = j->resident ? 1 : 0;
     return PHUB_OK;
 }
 
@@ -557,6 +575,7 @@ int phub_destroy(phub_job* j) {
     {
         std::lock_guard<std::mutex> lk(g_live_mu);
         if (!j || g_live.erase(j) == 0) return fail(PHUB_ESTATE, "not a live job handle");
+        if (j->cache_claim) g_cache_claimed[j->device] -= j->cache_claim;
     }
     DeviceScope ds(j->device);
     hipError_t e = hipStreamSynchronize(j->stream);

@@ -261,6 +261,36 @@ def test_all_keys_empty(lib, torch_dev):
     job.destroy()
 
 
+def test_default_cache_budget_is_shared(lib, torch_dev):
+    """Jobs created with the default option share a 256 MiB per-device
+    budget for cache-resident W and M, first come first served; destroying
+    a job gives its share back; an explicit budget is the job's own."""
+    torch, dev = torch_dev
+    elems = 75 << 18                     # W + M = 150 MiB
+    spec = Job("budget", 1, (elems,))
+    a = TorchJob(spec, dev, lib=lib)
+    b = TorchJob(spec, dev, lib=lib)
+    c = TorchJob(spec, dev, lib=lib, resident_bytes=1 << 40)
+    d = TorchJob(spec, dev, lib=lib, resident_bytes=0)
+    try:
+        assert a.info()[3] == 1
+        assert b.info()[3] == 0          # 300 MiB would exceed the budget
+        assert c.info()[3] == 1
+        assert d.info()[3] == 0
+        a.destroy()
+        a = None
+        e = TorchJob(spec, dev, lib=lib)
+        assert e.info()[3] == 1          # a's share came back
+        e.destroy()
+        tiny = TorchJob(Job("budget.tiny", 1, (1000,)), dev, lib=lib)
+        assert tiny.info()[3] == 1
+        tiny.destroy()
+    finally:
+        for j in (a, b, c, d):
+            if j is not None:
+                j.destroy()
+
+
 def test_set_weights_resets_momentum(lib, torch_dev):
     torch, dev = torch_dev
     job, res = run_small_case(torch, dev, lib, 2, [300], steps=2, seed=8)
