@@ -13,20 +13,19 @@
 // Launch shape: one workgroup of kBlockThreads per compute unit, persistent.
 // The step is HBM-bound and mixes many read streams with two in-place write
 // streams (W and M); on MI355X such a mix reaches the highest bandwidth with
-// few waves per CU, each keeping many bytes in flight, rather than with many
-// small workgroups.
+// few waves per CU.
 //
-// Memory access: a wave's hot loop moves one tile per iteration, 1024
-// elements of each of the N + 2 arrays: a lane loads 4 float4 of each
-// (the wave's 64 lanes cover 4 contiguous 1 KB pieces), all 4 * N gradient
-// loads in flight before the first addition.  Segments are cut on the host
-// into full tiles and a remainder, so the hot loop is straight-line code.
-// Gradients are read once per step and loaded non-temporally.  W and M are
-// read and written non-temporally, unless the job asks for them to stay in
-// the memory-side cache between steps (RES: default, cache-allocating
-// policy for every W and M access of the launch).  Tile descriptors and
-// per-key gradient pointers are uniform per wave and come through scalar
-// loads, prefetched two tiles ahead.
+// Memory access: a wave walks its full tiles, then its remainders.  A tile
+// is 1024 elements of each of the N + 2 arrays: a lane takes 4 float4 of
+// each (the wave's 64 lanes cover 4 contiguous 1 KB pieces).  Segments are
+// cut on the host into full tiles and a remainder, so the tile loop is
+// straight-line code.  The tile's loads go out piece by piece in a sliding
+// window that continues into the wave's next tile (see the load window
+// below); each piece is optimized and written back as soon as its last
+// gradient is in.  Gradients are read once per step and loaded
+// non-temporally.  W and M are read and written non-temporally, unless the
+// job keeps them in the memory-side cache between steps (RES: cache-
+// allocating policy for every W and M access of the launch).
 //
 // Arithmetic (no MFMA: the work is elementwise and HBM-bound): the sum is a
 // left fold in ascending worker index, plain fp32 additions; then four
