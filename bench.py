@@ -29,7 +29,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCES = ["paper_1805_07891_amd/csrc/fused_step.hip", "paper_1805_07891_amd/csrc/kernels.hpp"]
+# Sources that decide what the measured kernel reads and writes: the kernel
+# itself and the host code that builds its schedule and tables.
+KERNEL_SOURCES = ["paper_1805_07891_amd/csrc/fused_step.hip", "paper_1805_07891_amd/csrc/kernels.hpp",
+                  "paper_1805_07891_amd/csrc/plan.cpp", "paper_1805_07891_amd/csrc/plan.hpp",
+                  "paper_1805_07891_amd/csrc/phub_api.cpp"]
 DEFAULT_WORKLOAD = "resnet50"
 
 

@@ -39,8 +39,16 @@
 #ifndef PHUB_DEVICE_CACHE_BYTES
 #define PHUB_DEVICE_CACHE_BYTES (int64_t(256) << 20)
 #endif
-// The LPT schedule refines chunks until there are this many items per bin.
-constexpr int kLptItemsPerBin = 32;
+// The LPT schedule refines chunks until there are this many items per bin
+// (never below 1024 elements).  With ~1000 waves this yields one-tile items
+// for every workload up to ~130 M parameters: the waves then work on
+// neighbouring tiles at any moment, which keeps the window of addresses in
+// flight per array compact (measured: +2.6 points on a 102 M-parameter,
+// 16-worker job over two-tile items).
+#ifndef PHUB_LPT_ITEMS_PER_BIN
+#define PHUB_LPT_ITEMS_PER_BIN 128
+#endif
+constexpr int kLptItemsPerBin = PHUB_LPT_ITEMS_PER_BIN;
 
 namespace {
 
