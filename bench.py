@@ -81,6 +81,46 @@ def measured_traffic(workload: str):
     return rec.get("bytes_per_launch")
 
 
+NOTES = {
+    "tiny": "26.5 MB per step: W, M and gradients fit in the 256 MiB memory-side cache; "
+            "launch- and host-bound (host_us_per_step is the push and step calls)",
+}
+
+
+def read_ceiling(torch, dev, arenas, reps: int = 5):
+    """Measured HBM read ceiling of the same buffers in the same run: the
+    bandwidth probe (a read-only non-temporal stream, no arithmetic) over the
+    dominant job's gradient arenas; best of `reps` passes."""
+    import ctypes
+    from paper_1805_07891_amd import build as hip_build
+    if not os.path.exists(hip_build.PROBE_LIB):
+        raise RuntimeError(f"{hip_build.PROBE_LIB} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(hip_build.PROBE_LIB)
+    lib.phub_probe_read.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_int64,
+                                    ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+    lib.phub_probe_read.restype = ctypes.c_int
+    tile = lib.phub_probe_tile_elems()
+    n = min(a.numel() for a in arenas) // tile * tile
+    ptrs = (ctypes.c_void_p * len(arenas))(*[a.data_ptr() for a in arenas])
+    grid = torch.cuda.get_device_properties(dev).multi_processor_count
+    sink = torch.empty(grid * 256, dtype=torch.float32, device=dev)
+    stream = torch.cuda.Stream(device=dev)
+    best = 0.0
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        rc = lib.phub_probe_read(ptrs, len(arenas), n, grid, -1.2345678e30, ctypes.c_void_p(sink.data_ptr()),
+                                 ctypes.c_void_p(stream.cuda_stream))
+        e1.record(stream)
+        if rc != 0:
+            raise RuntimeError(f"phub_probe_read failed: {rc}")
+        torch.cuda.synchronize()
+        best = max(best, len(arenas) * n * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    return {"GBps": round(best, 1), "frac_of_peak": round(best / HBM_PEAK_GBS, 4),
+            "kind": "read-only non-temporal stream over the dominant job's gradient arenas",
+            "bytes": len(arenas) * n * 4}
+
+
 def cpu_baseline(wl, grads_dev, w0_dev, budget_s: float):
     """The oracle on the host, single-threaded, over the workload's first job
     (all keys) or a prefix of its keys, until `budget_s` seconds of work."""
@@ -128,7 +168,19 @@ def cpu_baseline(wl, grads_dev, w0_dev, budget_s: float):
                    f"{spec.num_params:,} params), N={spec.num_workers}, {steps} steps in "
                    f"{dt:.1f} s, one thread pinned to one core"),
         "host_cpus": os.cpu_count(),
+        "host_cpu_model": cpu_model(),
     }
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main(argv=None) -> int:
@@ -197,13 +249,16 @@ def main(argv=None) -> int:
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(K)] for _ in jobs]
     torch.cuda.synchronize()
+    host_s = 0.0
     t0 = time.perf_counter()
     for s in range(K):
+        h0 = time.perf_counter()
         for j, job in enumerate(jobs):
             job.push_all()
             ev[j][s][0].record(job.stream)
             job.step()
             ev[j][s][1].record(job.stream)
+        host_s += time.perf_counter() - h0
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
@@ -214,13 +269,16 @@ def main(argv=None) -> int:
 
     # dominant kernel: the job with the most bytes per launch
     dom = max(range(len(jobs)), key=lambda j: wl.jobs[j].hbm_bytes_per_step())
-    durs = [ev[dom][s][0].elapsed_time(ev[dom][s][1]) for s in range(K)]
+    durs = sorted(ev[dom][s][0].elapsed_time(ev[dom][s][1]) for s in range(K))
     avg_ms = sum(durs) / len(durs)
+    med_ms = durs[len(durs) // 2]
     dom_bytes = wl.jobs[dom].hbm_bytes_per_step()
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
     traffic = measured_traffic(args.workload)
     groups, threads, segs, _ = jobs[dom].info()
     cache_resident = [job.info()[3] for job in jobs]
+
+    ceiling = read_ceiling(torch, dev, grads[dom])
 
     baseline = None
     if args.cpu_seconds > 0:
@@ -250,6 +308,8 @@ def main(argv=None) -> int:
             "hbm_bytes_per_step": wl.hbm_bytes_per_step(),
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},
+            "host_us_per_step": round(host_s * 1e6 / K, 2),
+            "note": NOTES.get(args.workload, ""),
         },
         "roofline": {
             "bound": "hbm",
@@ -260,6 +320,10 @@ def main(argv=None) -> int:
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "avg_launch_us": round(avg_ms * 1e3, 2),
+            "median_launch_us": round(med_ms * 1e3, 2),
+            "min_launch_us": round(durs[0] * 1e3, 2),
+            "measured_read_ceiling": ceiling,
+            "frac_of_read_ceiling": round(achieved / ceiling["GBps"], 4),
             "algorithmic_bytes_per_launch": dom_bytes,
             "kernel_source_hash": kernel_source_hash(),
         },

@@ -1,4 +1,6 @@
-"""Builds the HIP library ``libphub.so`` in-tree for gfx950.
+"""Builds the HIP libraries in-tree for gfx950: ``libphub.so`` (the
+exchange step and its C interface) and ``libphub_probe.so`` (the bandwidth
+probe that the benchmark times beside the step).
 
 Every source is compiled by hipcc with contraction off, no fast-math and
 subnormals kept, so that the kernel performs exactly the fp32 operations
@@ -17,6 +19,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libphub.so")
+PROBE_LIB = os.path.join(PKG, "libphub_probe.so")
+PROBE_SOURCES = ["probe.hip"]
 
 SOURCES = ["plan.cpp", "phub_api.cpp", "fused_step.hip"]
 HEADERS = ["plan.hpp", "kernels.hpp"]
@@ -52,6 +56,23 @@ def build(out: str = LIB, defines: Sequence[str] = (), extra: Sequence[str] = ()
     return out
 
 
+def build_probe(out: str = PROBE_LIB, verbose: bool = False) -> str:
+    """Compile the bandwidth probe library; returns its path."""
+    srcs = [os.path.join(CSRC, s) for s in PROBE_SOURCES]
+    tmp = out + ".tmp"
+    cmd = [HIPCC, *FLAGS, f"-I{INCLUDE}", *srcs, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(tmp, out)
+    return out
+
+
+def build_all(verbose: bool = False) -> None:
+    build(verbose=verbose)
+    build_probe(verbose=verbose)
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    build_all(verbose=True)
     sys.exit(0)

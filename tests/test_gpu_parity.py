@@ -291,6 +291,34 @@ def test_default_cache_budget_is_shared(lib, torch_dev):
                 j.destroy()
 
 
+def test_bandwidth_probe_reads_and_leaves_sink(torch_dev):
+    """The probe runs on a small set of buffers, rejects bad arguments, and
+    writes the sink only where a sum hits the sentinel."""
+    import ctypes
+    torch, dev = torch_dev
+    from paper_1805_07891_amd import build
+    probe = ctypes.CDLL(build.PROBE_LIB)
+    probe.phub_probe_read.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_int64,
+                                      ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+    tile = probe.phub_probe_tile_elems()
+    bufs = [torch.ones(tile * 3, device=dev) for _ in range(3)]
+    ptrs = (ctypes.c_void_p * 3)(*[b.data_ptr() for b in bufs])
+    sink = torch.zeros(8 * 256, device=dev)
+    _say("probe: 3 buffers of", tile * 3, "floats, grid 8")
+    assert probe.phub_probe_read(ptrs, 3, tile * 3, 8, -7.0, ctypes.c_void_p(sink.data_ptr()), None) == 0
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(sink).item() == 0
+    assert probe.phub_probe_read(ptrs, 3, tile * 3 + 1, 8, -7.0, ctypes.c_void_p(sink.data_ptr()), None) == -1
+    assert probe.phub_probe_read(ptrs, 0, tile, 8, -7.0, ctypes.c_void_p(sink.data_ptr()), None) == -1
+    # a sentinel the data does hit: every lane of a wave that read one tile of
+    # ones sums 4 * 8 = 32 per tile it read
+    one = (ctypes.c_void_p * 1)(bufs[0].data_ptr())
+    assert probe.phub_probe_read(one, 1, tile, 1, 32.0, ctypes.c_void_p(sink.data_ptr()), None) == 0
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(sink[:64]).item() == 64      # wave 0 read the single tile
+    assert torch.count_nonzero(sink[64:]).item() == 0
+
+
 def test_set_weights_resets_momentum(lib, torch_dev):
     torch, dev = torch_dev
     job, res = run_small_case(torch, dev, lib, 2, [300], steps=2, seed=8)

@@ -12,6 +12,8 @@ import os
 import re
 
 import numpy as np
+import subprocess
+
 import pytest
 
 from paper_1805_07891_amd import phub, workloads
@@ -37,6 +39,26 @@ def test_header_symbols_are_exported(lib):
     assert declared == set(phub.EXPORTED)
     for name in declared:
         assert hasattr(lib.lib, name), name
+
+
+def test_probe_header_symbols_are_exported():
+    """The bandwidth probe library exports exactly what its header declares
+    (loaded without calling anything: no GPU here)."""
+    import ctypes
+    from paper_1805_07891_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        build.build_probe()
+    with open(os.path.join(ROOT, "include", "phub_probe.h")) as f:
+        text = f.read()
+    declared = set(re.findall(r"^\s*int\s*(phub_\w+)\s*\(", text, re.M))
+    assert declared == {"phub_probe_read", "phub_probe_tile_elems"}
+    probe = ctypes.CDLL(build.PROBE_LIB)
+    for name in declared:
+        assert hasattr(probe, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", build.PROBE_LIB], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {ln.split()[-1] for ln in out.splitlines() if " T " in ln and "phub_" in ln}
+    assert exported == declared
 
 
 LPT = phub.PHUB_SCHEDULE_LPT
