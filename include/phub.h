@@ -104,6 +104,20 @@ typedef struct phub_options {
                                first served by the live jobs created with -1
                                and given back by phub_destroy.  Results do
                                not depend on it. */
+    int num_groups;         /* readiness groups (sections 3.2.2-3.2.3: a
+                               chunk is aggregated as soon as all of its
+                               pieces have arrived).  0: none; the whole step
+                               is enqueued by phub_step.  > 0: key k belongs
+                               to group key_group[k]; as soon as every worker
+                               has pushed every key of a group, that group's
+                               aggregation and update are enqueued on the
+                               job's stream (after a device-side wait on the
+                               ready events of its pushes), while later
+                               groups are still being pushed.  Results do not
+                               depend on the grouping. */
+    const int *key_group;   /* num_keys entries in [0, num_groups), read
+                               during phub_init_ex only; ignored when
+                               num_groups is 0. */
 } phub_options;
 
 /*
@@ -132,10 +146,25 @@ int phub_set_weights(phub_job *job, int key, const float *src);
  *          on the job's stream.
  * Nothing is copied: the pointer is recorded for the next phub_step.  The
  * worker index, not the call order, fixes the worker's place in the sum.
- * Pushing a pair again before the step replaces the earlier pointer.
- * Errors: PHUB_EINVAL (range, null, alignment), PHUB_ESTATE.
+ * Pushing a pair again before the step replaces the earlier pointer.  With
+ * readiness groups, the push that completes a group enqueues that group's
+ * work (see phub_options.num_groups); pushing a key of a group that has
+ * already been enqueued in this step is PHUB_ESTATE.
+ * Errors: PHUB_EINVAL (range, null, alignment), PHUB_ESTATE, PHUB_EHIP (an
+ * enqueue triggered by the push failed).
  */
 int phub_push(phub_job *job, int worker, int key, const float *grad);
+
+/*
+ * phub_push_event - phub_push for a gradient that is still being produced:
+ * it is ready once `hip_event` (a hipEvent_t recorded by the producer on its
+ * own stream; NULL = ready now) has completed.  The step's work that reads
+ * this gradient waits for the event on the device (hipStreamWaitEvent on the
+ * job's stream); the host never blocks on it.  The event must stay valid
+ * until that work is enqueued: when its readiness group completes, at the
+ * latest at phub_step.  Same rules and errors as phub_push.
+ */
+int phub_push_event(phub_job *job, int worker, int key, const float *grad, void *hip_event);
 
 /*
  * phub_push_keys - batched phub_push for one worker: pushes grads[i] for key
@@ -151,7 +180,13 @@ int phub_push_keys(phub_job *job, int worker, int count, const int *keys,
  * host.  Requires every (worker, key) pair to have been pushed since the
  * previous step, else PHUB_ENOTREADY and nothing is enqueued.  If a pushed
  * pointer differs from the last step's, the pointer table is uploaded on the
- * same stream first.  Afterwards all pairs count as not pushed.
+ * same stream first; the launch first waits for the ready events given to
+ * phub_push_event.  Afterwards all pairs count as not pushed.
+ * With readiness groups, the groups were enqueued as they completed; the
+ * step enqueues any group without keys, closes the step, and reports
+ * PHUB_ENOTREADY (enqueuing nothing more) while a pair is missing: the groups
+ * already enqueued stay applied, and the step completes once the missing
+ * pushes arrive and phub_step is called again.
  * Errors: PHUB_ENOTREADY, PHUB_ESTATE, PHUB_EHIP.
  */
 int phub_step(phub_job *job);

@@ -27,7 +27,7 @@ constexpr int64_t kTileElems = 64 * 4 * kVecPerLane;
 // element 4 * vec.
 struct DevTile {
     int64_t arena_offset;  // index of the tile's first element in the W and M arenas
-    int32_t key;
+    int32_t key;           // the key's row in the gradient pointer table
     int32_t vec;           // index of the tile's first float4 within the key
 };
 static_assert(sizeof(DevTile) == 16, "DevTile layout");
@@ -37,7 +37,7 @@ static_assert(sizeof(DevTile) == 16, "DevTile layout");
 struct DevRem {
     int64_t arena_offset;  // index of the first element in the W and M arenas
     int64_t offset;        // index of the first element within the key (multiple of 4)
-    int32_t key;
+    int32_t key;           // the key's row in the gradient pointer table
     int32_t count;         // elements, 1 .. kTileElems - 1
     int64_t pad;
 };
@@ -48,7 +48,7 @@ struct StepParams {
     const int32_t* tile_begin;    // wave w owns tiles [tile_begin[w], tile_begin[w+1])
     const DevRem* rems;           // grouped by bin
     const int32_t* rem_begin;     // wave w owns rems [rem_begin[w], rem_begin[w+1])
-    const float* const* grads;    // [key * num_workers + worker], 16-byte aligned
+    const float* const* grads;    // [row * num_workers + worker], 16-byte aligned
     float* weights;               // W arena
     float* moments;               // M arena
     float lr;

@@ -7,6 +7,15 @@
 // stream its work is ordered on.  A push only records a pointer (the
 // zero-copy registration of section 3.2.1); a step uploads the pointer table
 // if it changed and launches one fused kernel for all keys.
+//
+// Readiness groups (sections 3.2.2-3.2.3: PHub aggregates a chunk as soon
+// as all of its pieces have arrived, overlapping reception with
+// aggregation): a job may partition its keys into groups at creation.  Each
+// group has its own schedule, and the fused kernel for a group is enqueued
+// as soon as every worker has pushed every key of the group, after waiting
+// on the device for the ready events given with the pushes.  The pointer
+// table is laid out by group (keys of a group on consecutive rows), so a
+// group uploads only its own rows.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -93,31 +102,47 @@ struct phub_job {
     bool own_stream = false;
 
     int schedule = phub::kScheduleLpt;
-    int groups = 0;  // workgroups of one launch
+    int groups = 0;  // workgroups of one launch (0: no key has elements)
     int bins = 0;    // waves with a segment list (groups * waves per workgroup)
     int64_t num_segments = 0;
     int64_t num_tiles = 0;
     int64_t num_rems = 0;
-    bool resident = false;  // W and M stay in the memory-side cache between steps
+    bool resident = false;    // W and M stay in the memory-side cache between steps
     int64_t cache_claim = 0;  // bytes of the device's default cache budget this job holds
+
+    // Readiness groups.  Without groups the job has one group holding every
+    // key, launched by phub_step.
+    bool streaming = false;              // groups launch as soon as they are complete
+    int num_rgroups = 1;
+    std::vector<int> key_rgroup;         // per key
+    std::vector<int> row_of_key;         // pointer-table row of each key
+    std::vector<int> key_of_row;
+    std::vector<int> rgroup_row_begin;   // rows of group g: [begin[g], begin[g + 1])
+    std::vector<uint8_t> rgroup_work;    // the group's schedule has segments
+    std::vector<int64_t> rgroup_pushed;  // (worker, key) pairs pushed this step
+    std::vector<uint8_t> rgroup_launched;
+    std::vector<uint8_t> rgroup_dirty;   // its rows changed since they were last uploaded
 
     float* weights = nullptr;
     float* moments = nullptr;
     phub::DevTile* d_tiles = nullptr;
-    int32_t* d_tile_begin = nullptr;
+    int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of bins + 1 entries
     phub::DevRem* d_rems = nullptr;
-    int32_t* d_rem_begin = nullptr;
-    const float** d_grads = nullptr;
+    int32_t* d_rem_begin = nullptr;   // same layout
+    const float** d_grads = nullptr;  // [row * N + worker]
 
-    std::vector<const float*> grads;  // host table, [key * N + worker]
+    std::vector<const float*> grads;  // host table, [row * N + worker]
+    std::vector<hipEvent_t> ready;    // same layout: event to wait for (none if null)
     std::vector<uint8_t> pushed;      // same layout: pushed since the last step
     int64_t num_pushed = 0;
-    bool table_dirty = true;          // host table differs from the device copy
 
+    // Pinned staging of the pointer table: one slot per step, reused after
+    // kStageSlots steps once the copies that read it have run.
     const float** stage[kStageSlots] = {};
     hipEvent_t stage_done[kStageSlots] = {};
     bool stage_used[kStageSlots] = {};
-    int stage_next = 0;
+    int stage_slot = 0;
+    bool stage_claimed = false;  // this step has waited for its slot
 };
 
 namespace {
@@ -176,37 +201,100 @@ int check_grad(const phub_job* j, int worker, int key, const float* grad) {
     if (reinterpret_cast<uintptr_t>(grad) % 16 != 0)
         return fail(PHUB_EINVAL, "gradient of worker %d for key %d is not 16-byte aligned", worker,
                     key);
+    if (j->streaming && j->rgroup_launched[j->key_rgroup[key]])
+        return fail(PHUB_ESTATE,
+                    "key %d belongs to readiness group %d, which was already launched this step",
+                    key, j->key_rgroup[key]);
     return PHUB_OK;
 }
 
-void record_push(phub_job* j, int worker, int key, const float* grad) {
-    const size_t i = size_t(key) * j->num_workers + worker;
+// Copies the rows of group g from the host table to the device, through the
+// current step's pinned staging slot, on the job's stream.
+int upload_rows(phub_job* j, int g) {
+    const int slot = j->stage_slot;
+    if (!j->stage_claimed) {
+        if (j->stage_used[slot]) {
+            hipError_t e = hipEventSynchronize(j->stage_done[slot]);
+            if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize (pointer staging)");
+        }
+        j->stage_claimed = true;
+    }
+    const size_t n = size_t(j->num_workers);
+    const size_t r0 = size_t(j->rgroup_row_begin[g]) * n;
+    const size_t r1 = size_t(j->rgroup_row_begin[g + 1]) * n;
+    if (r1 > r0) {
+        std::memcpy(j->stage[slot] + r0, j->grads.data() + r0, (r1 - r0) * sizeof(const float*));
+        hipError_t e = hipMemcpyAsync(j->d_grads + r0, j->stage[slot] + r0,
+                                      (r1 - r0) * sizeof(const float*), hipMemcpyHostToDevice,
+                                      j->stream);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pointer table)");
+        e = hipEventRecord(j->stage_done[slot], j->stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (pointer staging)");
+        j->stage_used[slot] = true;
+    }
+    j->rgroup_dirty[g] = 0;
+    return PHUB_OK;
+}
+
+// Enqueues group g: its pointer rows if they changed, a wait for every
+// distinct ready event of its pushes, then the fused kernel over its
+// schedule.
+int launch_group(phub_job* j, int g) {
+    DeviceScope ds(j->device);
+    if (!ds.ok()) return fail(PHUB_EHIP, "cannot make device %d current", j->device);
+    if (j->rgroup_dirty[g])
+        if (int rc = upload_rows(j, g)) return rc;
+    const size_t n = size_t(j->num_workers);
+    std::vector<hipEvent_t> evs;
+    for (size_t i = size_t(j->rgroup_row_begin[g]) * n; i < size_t(j->rgroup_row_begin[g + 1]) * n;
+         ++i)
+        if (j->ready[i]) evs.push_back(j->ready[i]);
+    std::sort(evs.begin(), evs.end());
+    evs.erase(std::unique(evs.begin(), evs.end()), evs.end());
+    for (hipEvent_t ev : evs) {
+        hipError_t e = hipStreamWaitEvent(j->stream, ev, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent (ready event)");
+    }
+    if (j->rgroup_work[g]) {
+        phub::StepParams p;
+        p.tiles = j->d_tiles;
+        p.tile_begin = j->d_tile_begin + size_t(g) * (j->bins + 1);
+        p.rems = j->d_rems;
+        p.rem_begin = j->d_rem_begin + size_t(g) * (j->bins + 1);
+        p.grads = j->d_grads;
+        p.weights = j->weights;
+        p.moments = j->moments;
+        p.lr = j->lr;
+        p.mu = j->mu;
+        p.wd = j->wd;
+        p.num_workers = j->num_workers;
+        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->resident, j->groups, j->stream);
+        if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
+    }
+    j->rgroup_launched[g] = 1;
+    return PHUB_OK;
+}
+
+int record_push(phub_job* j, int worker, int key, const float* grad, hipEvent_t ev) {
+    const int g = j->key_rgroup[key];
+    if (j->streaming && j->rgroup_launched[g])  // e.g. a key repeated in one batch
+        return fail(PHUB_ESTATE,
+                    "key %d belongs to readiness group %d, which was already launched this step",
+                    key, g);
+    const size_t i = size_t(j->row_of_key[key]) * j->num_workers + worker;
     if (j->grads[i] != grad) {
         j->grads[i] = grad;
-        j->table_dirty = true;
+        j->rgroup_dirty[g] = 1;
     }
+    j->ready[i] = ev;
     if (!j->pushed[i]) {
         j->pushed[i] = 1;
         ++j->num_pushed;
+        ++j->rgroup_pushed[g];
+        const int64_t need =
+            int64_t(j->rgroup_row_begin[g + 1] - j->rgroup_row_begin[g]) * j->num_workers;
+        if (j->streaming && j->rgroup_pushed[g] == need) return launch_group(j, g);
     }
-}
-
-int upload_table(phub_job* j) {
-    const int slot = j->stage_next;
-    const size_t bytes = j->grads.size() * sizeof(const float*);
-    if (j->stage_used[slot]) {
-        hipError_t e = hipEventSynchronize(j->stage_done[slot]);
-        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize (pointer staging)");
-    }
-    std::memcpy(j->stage[slot], j->grads.data(), bytes);
-    hipError_t e = hipMemcpyAsync(j->d_grads, j->stage[slot], bytes, hipMemcpyHostToDevice,
-                                  j->stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pointer table)");
-    e = hipEventRecord(j->stage_done[slot], j->stream);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord (pointer staging)");
-    j->stage_used[slot] = true;
-    j->stage_next = (slot + 1) % kStageSlots;
-    j->table_dirty = false;
     return PHUB_OK;
 }
 
@@ -275,14 +363,25 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         return fail(PHUB_EINVAL, "lr, momentum and weight_decay must be finite");
     int schedule = phub::kScheduleLpt;
     int64_t resident_bytes = -1;  // -1: the shared per-device budget
+    int num_rgroups = 0;          // 0: no readiness groups
     if (options) {
         if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
         if (options->resident_bytes < -1)
             return fail(PHUB_EINVAL, "resident_bytes must be >= -1, got %lld",
                         (long long)options->resident_bytes);
+        if (options->num_groups < 0)
+            return fail(PHUB_EINVAL, "num_groups must be >= 0, got %d", options->num_groups);
+        if (options->num_groups > 0) {
+            if (!options->key_group) return fail(PHUB_EINVAL, "key_group is NULL");
+            for (int k = 0; k < num_keys; ++k)
+                if (options->key_group[k] < 0 || options->key_group[k] >= options->num_groups)
+                    return fail(PHUB_EINVAL, "key_group[%d] = %d is outside [0, %d)", k,
+                                options->key_group[k], options->num_groups);
+        }
         schedule = options->schedule;
         if (options->resident_bytes >= 0) resident_bytes = options->resident_bytes;
+        num_rgroups = options->num_groups;
     }
 
     phub_job* j = new (std::nothrow) phub_job;
@@ -303,7 +402,28 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->wd = weight_decay;
         j->nesterov = nesterov != 0;
         j->grads.assign(size_t(num_workers) * num_keys, nullptr);
+        j->ready.assign(size_t(num_workers) * num_keys, nullptr);
         j->pushed.assign(size_t(num_workers) * num_keys, 0);
+        // readiness groups; rows of the pointer table ordered by group, then key
+        j->streaming = num_rgroups > 0;
+        j->num_rgroups = j->streaming ? num_rgroups : 1;
+        j->key_rgroup.assign(num_keys, 0);
+        if (j->streaming) j->key_rgroup.assign(options->key_group, options->key_group + num_keys);
+        j->rgroup_row_begin.assign(j->num_rgroups + 1, 0);
+        for (int k = 0; k < num_keys; ++k) ++j->rgroup_row_begin[j->key_rgroup[k] + 1];
+        for (int g = 0; g < j->num_rgroups; ++g) j->rgroup_row_begin[g + 1] += j->rgroup_row_begin[g];
+        j->row_of_key.assign(num_keys, 0);
+        j->key_of_row.assign(num_keys, 0);
+        std::vector<int> next(j->rgroup_row_begin.begin(), j->rgroup_row_begin.end() - 1);
+        for (int k = 0; k < num_keys; ++k) {
+            const int row = next[j->key_rgroup[k]]++;
+            j->row_of_key[k] = row;
+            j->key_of_row[row] = k;
+        }
+        j->rgroup_work.assign(j->num_rgroups, 0);
+        j->rgroup_pushed.assign(j->num_rgroups, 0);
+        j->rgroup_launched.assign(j->num_rgroups, 0);
+        j->rgroup_dirty.assign(j->num_rgroups, 1);
     } catch (const std::bad_alloc&) {
         delete j;
         return fail(PHUB_ENOMEM, "host allocation of the job tables failed");
@@ -322,14 +442,31 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                                : fail(PHUB_EHIP, "device reports no compute units");
     }
 
-    phub::Plan plan;
+    // One schedule per readiness group, over the group's keys in row order.
+    std::vector<phub::Plan> plans;
     {
         const int groups = cus * PHUB_GROUPS_PER_CU;
         const int bins = groups * (phub::kBlockThreads / 64);
         std::string err;
         try {
-            err = phub::build_plan(num_workers, num_keys, key_elems, chunk_bytes, schedule, bins,
-                                   kLptItemsPerBin * bins, &plan);
+            plans.resize(j->num_rgroups);
+            for (int g = 0; g < j->num_rgroups && err.empty(); ++g) {
+                const int r0 = j->rgroup_row_begin[g], r1 = j->rgroup_row_begin[g + 1];
+                phub::Plan& plan = plans[g];
+                if (r1 > r0) {
+                    std::vector<int64_t> elems(r1 - r0);
+                    for (int r = r0; r < r1; ++r) elems[r - r0] = key_elems[j->key_of_row[r]];
+                    err = phub::build_plan(num_workers, r1 - r0, elems.data(), chunk_bytes,
+                                           schedule, bins, kLptItemsPerBin * bins, &plan);
+                } else {
+                    plan.bin_begin.assign(1, 0);
+                }
+                // every wave of the grid reads its bin: pad dropped bins as empty
+                while (plan.bin_begin.size() < size_t(bins) + 1)
+                    plan.bin_begin.push_back(plan.bin_begin.back());
+                j->rgroup_work[g] = plan.segments.empty() ? 0 : 1;
+                j->num_segments += int64_t(plan.segments.size());
+            }
         } catch (const std::bad_alloc&) {
             delete j;
             return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
@@ -338,13 +475,10 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             delete j;
             return fail(PHUB_EINVAL, "%s", err.c_str());
         }
-        // every wave of the grid reads its bin: pad dropped bins as empty
-        while (plan.bin_begin.size() < size_t(bins) + 1) plan.bin_begin.push_back(plan.bin_begin.back());
-        j->groups = plan.segments.empty() ? 0 : groups;
+        j->groups = j->num_segments == 0 ? 0 : groups;
         j->bins = bins;
     }
     j->schedule = schedule;
-    j->num_segments = int64_t(plan.segments.size());
     const int64_t wm_bytes = 2 * j->arena_elems * int64_t(sizeof(float));
     if (resident_bytes >= 0) j->resident = wm_bytes > 0 && wm_bytes <= resident_bytes;
 
@@ -375,32 +509,40 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         PHUB_TRY(hipMemsetAsync(j->weights, 0, arena_bytes, j->stream), "hipMemsetAsync(W)");
         PHUB_TRY(hipMemsetAsync(j->moments, 0, arena_bytes, j->stream), "hipMemsetAsync(M)");
 
-        // Device form of the schedule: each bin's segments become full tiles
+        // Device form of the schedules: each bin's segments become full tiles
         // (the kernel's straight-line hot loop) and at most one remainder
-        // each (partial tile and ragged end), in segment order.
+        // each (partial tile and ragged end), in segment order; one block of
+        // bin offsets per readiness group.  A descriptor's key is the key's
+        // row in the pointer table.
         std::vector<phub::DevTile> dtiles;
         std::vector<phub::DevRem> drems;
-        std::vector<int32_t> tile_begin(1, 0), rem_begin(1, 0);
-        const int nb = int(plan.bin_begin.size()) - 1;
-        for (int b = 0; b < nb; ++b) {
-            for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
-                const phub::PlanSegment& sg = plan.segments[i];
-                const int64_t ao = j->arena_offset[sg.key] + sg.offset;
-                const int64_t nfull = sg.count / phub::kTileElems;
-                for (int64_t t = 0; t < nfull; ++t)
-                    dtiles.push_back({ao + t * phub::kTileElems, sg.key,
-                                      int32_t((sg.offset + t * phub::kTileElems) / 4)});
-                const int64_t done = nfull * phub::kTileElems;
-                if (done < sg.count)
-                    drems.push_back({ao + done, sg.offset + done, sg.key,
-                                     int32_t(sg.count - done), 0});
-            }
-            if (dtiles.size() > size_t(INT32_MAX) || drems.size() > size_t(INT32_MAX)) {
-                rc = fail(PHUB_EINVAL, "schedule too large");
-                goto fail_cleanup;
-            }
+        std::vector<int32_t> tile_begin, rem_begin;
+        for (int g = 0; g < j->num_rgroups; ++g) {
+            const phub::Plan& plan = plans[g];
+            const int row0 = j->rgroup_row_begin[g];
             tile_begin.push_back(int32_t(dtiles.size()));
             rem_begin.push_back(int32_t(drems.size()));
+            for (int b = 0; b < j->bins; ++b) {
+                for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
+                    const phub::PlanSegment& sg = plan.segments[i];
+                    const int row = row0 + sg.key;
+                    const int64_t ao = j->arena_offset[j->key_of_row[row]] + sg.offset;
+                    const int64_t nfull = sg.count / phub::kTileElems;
+                    for (int64_t t = 0; t < nfull; ++t)
+                        dtiles.push_back({ao + t * phub::kTileElems, row,
+                                          int32_t((sg.offset + t * phub::kTileElems) / 4)});
+                    const int64_t done = nfull * phub::kTileElems;
+                    if (done < sg.count)
+                        drems.push_back({ao + done, sg.offset + done, row,
+                                         int32_t(sg.count - done), 0});
+                }
+                if (dtiles.size() > size_t(INT32_MAX) || drems.size() > size_t(INT32_MAX)) {
+                    rc = fail(PHUB_EINVAL, "schedule too large");
+                    goto fail_cleanup;
+                }
+                tile_begin.push_back(int32_t(dtiles.size()));
+                rem_begin.push_back(int32_t(drems.size()));
+            }
         }
         j->num_tiles = int64_t(dtiles.size());
         j->num_rems = int64_t(drems.size());
@@ -482,10 +624,13 @@ int phub_set_weights(phub_job* j, int key, const float* src) {
 }
 
 int phub_push(phub_job* j, int worker, int key, const float* grad) {
+    return phub_push_event(j, worker, key, grad, nullptr);
+}
+
+int phub_push_event(phub_job* j, int worker, int key, const float* grad, void* hip_event) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     if (int rc = check_grad(j, worker, key, grad)) return rc;
-    record_push(j, worker, key, grad);
-    return PHUB_OK;
+    return record_push(j, worker, key, grad, static_cast<hipEvent_t>(hip_event));
 }
 
 int phub_push_keys(phub_job* j, int worker, int count, const int* keys,
@@ -497,7 +642,8 @@ int phub_push_keys(phub_job* j, int worker, int count, const int* keys,
         return fail(PHUB_EINVAL, "count %d exceeds the %d keys", count, j->num_keys);
     for (int i = 0; i < count; ++i)
         if (int rc = check_grad(j, worker, keys ? keys[i] : i, grads[i])) return rc;
-    for (int i = 0; i < count; ++i) record_push(j, worker, keys ? keys[i] : i, grads[i]);
+    for (int i = 0; i < count; ++i)
+        if (int rc = record_push(j, worker, keys ? keys[i] : i, grads[i], nullptr)) return rc;
     return PHUB_OK;
 }
 
@@ -505,35 +651,26 @@ int phub_step(phub_job* j) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     const int64_t need = int64_t(j->num_workers) * j->num_keys;
     if (j->num_pushed != need) {
-        for (size_t i = 0; i < j->pushed.size(); ++i)
-            if (!j->pushed[i])
-                return fail(PHUB_ENOTREADY,
-                            "%lld of %lld (worker, key) pairs pushed; worker %d has not pushed key %d",
-                            (long long)j->num_pushed, (long long)need, int(i % j->num_workers),
-                            int(i / j->num_workers));
+        for (int k = 0; k < j->num_keys; ++k)
+            for (int w = 0; w < j->num_workers; ++w)
+                if (!j->pushed[size_t(j->row_of_key[k]) * j->num_workers + w])
+                    return fail(PHUB_ENOTREADY,
+                                "%lld of %lld (worker, key) pairs pushed; worker %d has not "
+                                "pushed key %d",
+                                (long long)j->num_pushed, (long long)need, w, k);
     }
-    DeviceScope ds(j->device);
-    if (!ds.ok()) return fail(PHUB_EHIP, "cannot make device %d current", j->device);
-    if (j->table_dirty)
-        if (int rc = upload_table(j)) return rc;
-    if (j->groups > 0) {
-        phub::StepParams p;
-        p.tiles = j->d_tiles;
-        p.tile_begin = j->d_tile_begin;
-        p.rems = j->d_rems;
-        p.rem_begin = j->d_rem_begin;
-        p.grads = j->d_grads;
-        p.weights = j->weights;
-        p.moments = j->moments;
-        p.lr = j->lr;
-        p.mu = j->mu;
-        p.wd = j->wd;
-        p.num_workers = j->num_workers;
-        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->resident, j->groups, j->stream);
-        if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
-    }
+    for (int g = 0; g < j->num_rgroups; ++g)
+        if (!j->rgroup_launched[g])
+            if (int rc = launch_group(j, g)) return rc;
     std::fill(j->pushed.begin(), j->pushed.end(), 0);
+    std::fill(j->ready.begin(), j->ready.end(), nullptr);
+    std::fill(j->rgroup_pushed.begin(), j->rgroup_pushed.end(), 0);
+    std::fill(j->rgroup_launched.begin(), j->rgroup_launched.end(), 0);
     j->num_pushed = 0;
+    if (j->stage_claimed) {
+        j->stage_slot = (j->stage_slot + 1) % kStageSlots;
+        j->stage_claimed = false;
+    }
     return PHUB_OK;
 }
 

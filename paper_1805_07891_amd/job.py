@@ -55,7 +55,8 @@ class TorchJob:
 
     def __init__(self, spec: Job, device, stream=None, chunk_bytes: Optional[int] = None,
                  lib: Optional[_phub.Library] = None, schedule: Optional[int] = None,
-                 resident_bytes: Optional[int] = None):
+                 resident_bytes: Optional[int] = None,
+                 key_group: Optional[Sequence[int]] = None):
         import torch
         self.torch = torch
         self.spec = spec
@@ -68,7 +69,9 @@ class TorchJob:
             self.handle = self.lib.phub_init(spec.num_workers, spec.key_elems, self.chunk_bytes,
                                              spec.lr, spec.momentum, spec.weight_decay,
                                              spec.nesterov, self.stream.cuda_stream,
-                                             schedule=schedule, resident_bytes=resident_bytes)
+                                             schedule=schedule, resident_bytes=resident_bytes,
+                                             key_group=key_group)
+        self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers
         self._grad_refs: List = [None] * spec.num_workers
 
@@ -101,6 +104,16 @@ class TorchJob:
             if arr is None:
                 raise RuntimeError(f"worker {w} has no gradient arena attached")
             self.lib.phub_push_keys(self.handle, w, arr)
+
+    def push_key(self, worker: int, key: int, event=None) -> None:
+        """Push one key of worker ``worker`` from its attached arena; with
+        ``event`` (a torch.cuda.Event recorded by the producer) the gradient
+        counts as ready once the event completes."""
+        ptr = self.key_pointers(self._grad_refs[worker])[key]
+        if event is None:
+            self.lib.phub_push(self.handle, worker, key, ptr)
+        else:
+            self.lib.phub_push_event(self.handle, worker, key, ptr, event.cuda_event)
 
     def step(self) -> None:
         self.lib.phub_step(self.handle)

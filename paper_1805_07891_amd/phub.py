@@ -31,7 +31,8 @@ PHUB_SCHEDULE_SPLIT = 0
 PHUB_SCHEDULE_LPT = 1
 
 # Every symbol the header declares.
-EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_push_keys",
+EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_push_event",
+            "phub_push_keys",
             "phub_step", "phub_pull", "phub_get_state", "phub_sync", "phub_get_stream",
             "phub_job_info", "phub_destroy", "phub_last_error", "phub_plan_count",
             "phub_plan_build")
@@ -48,7 +49,8 @@ class PhubSegment(ctypes.Structure):
 
 
 class PhubOptions(ctypes.Structure):
-    _fields_ = [("schedule", ctypes.c_int), ("resident_bytes", ctypes.c_int64)]
+    _fields_ = [("schedule", ctypes.c_int), ("resident_bytes", ctypes.c_int64),
+                ("num_groups", ctypes.c_int), ("key_group", ctypes.POINTER(ctypes.c_int))]
 
 
 class Library:
@@ -67,6 +69,7 @@ class Library:
                               ctypes.POINTER(PhubOptions)], i32),
             "phub_set_weights": ([vp, i32, vp], i32),
             "phub_push": ([vp, i32, i32, vp], i32),
+            "phub_push_event": ([vp, i32, i32, vp, vp], i32),
             "phub_push_keys": ([vp, i32, i32, vp, vp], i32),
             "phub_step": ([vp], i32),
             "phub_pull": ([vp, i32, pp], i32),
@@ -99,20 +102,29 @@ class Library:
     def phub_init(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
                   lr: float, momentum: float, weight_decay: float, nesterov: bool,
                   hip_stream: Optional[int] = None, check: bool = True,
-                  schedule: Optional[int] = None, resident_bytes: Optional[int] = None):
+                  schedule: Optional[int] = None, resident_bytes: Optional[int] = None,
+                  key_group: Optional[Sequence[int]] = None, num_groups: Optional[int] = None):
         """Returns the job handle (an int), or (rc, None) with check=False on
-        error.  With ``schedule`` or ``resident_bytes`` given, calls
-        phub_init_ex with those options."""
+        error.  With ``schedule``, ``resident_bytes`` or readiness groups
+        (``key_group``: the group of each key; ``num_groups`` defaults to
+        max + 1) given, calls phub_init_ex with those options."""
         elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
         out = ctypes.c_void_p()
         args = (ctypes.byref(out), int(num_workers), len(key_elems),
                 ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes), float(lr), float(momentum),
                 float(weight_decay), int(bool(nesterov)), hip_stream)
-        if schedule is None and resident_bytes is None:
+        if schedule is None and resident_bytes is None and key_group is None and num_groups is None:
             rc = self.lib.phub_init(*args)
         else:
+            groups = None
+            if key_group is not None:
+                groups = (ctypes.c_int * max(len(key_group), 1))(*[int(g) for g in key_group])
+                if num_groups is None:
+                    num_groups = max((int(g) for g in key_group), default=-1) + 1
             opts = PhubOptions(PHUB_SCHEDULE_LPT if schedule is None else int(schedule),
-                               -1 if resident_bytes is None else int(resident_bytes))
+                               -1 if resident_bytes is None else int(resident_bytes),
+                               0 if num_groups is None else int(num_groups),
+                               ctypes.cast(groups, ctypes.POINTER(ctypes.c_int)) if groups else None)
             rc = self.lib.phub_init_ex(*args, ctypes.byref(opts))
         if rc != 0:
             self._check(rc, check)
@@ -124,6 +136,12 @@ class Library:
 
     def phub_push(self, job, worker: int, key: int, grad_ptr: int, check: bool = True) -> int:
         return self._check(self.lib.phub_push(job, int(worker), int(key), grad_ptr), check)
+
+    def phub_push_event(self, job, worker: int, key: int, grad_ptr: int, hip_event: Optional[int],
+                        check: bool = True) -> int:
+        """hip_event: a hipEvent_t handle as an int (torch.cuda.Event.cuda_event) or None."""
+        return self._check(self.lib.phub_push_event(job, int(worker), int(key), grad_ptr, hip_event),
+                           check)
 
     def phub_push_keys(self, job, worker: int, grad_ptrs, keys=None, check: bool = True) -> int:
         """grad_ptrs: a ctypes c_void_p array (see ``pointer_array``) or a
