@@ -172,6 +172,144 @@ def cpu_baseline(wl, grads_dev, w0_dev, budget_s: float):
     }
 
 
+def readiness_groups(spec, bucket_bytes: float):
+    """Keys grouped in backward order (last key first) into runs of at
+    least `bucket_bytes` of fp32 gradient per worker; group 0 holds the last
+    keys, which the backward pass produces first."""
+    group = [0] * spec.num_keys
+    g, acc = 0, 0
+    for k in reversed(range(spec.num_keys)):
+        group[k] = g
+        acc += spec.key_elems[k] * 4
+        if acc >= bucket_bytes:
+            g, acc = g + 1, 0
+    return group, g + (1 if acc > 0 else 0)
+
+
+def streaming_bench(torch, dev, lib, wl, args) -> int:
+    """The step overlapped with a simulated backward pass that produces the
+    gradients (sections 3.2.2-3.2.3: a chunk is aggregated as soon as all of
+    its pieces have arrived).  Every worker has its own stream and delivers its keys in
+    backward order (last key first), in buckets of --producer-mb, one event
+    per bucket; the host pushes each bucket's keys with that event at once.
+    Each bucket is first computed on the same GPU (bf16 GEMMs proportional
+    to the bucket's parameters: the layers' backward work), then written.
+    Timed on the device from the start of the backward to the end of the
+    step, for one launch at phub_step and for readiness groups of
+    --bucket-mb launched as they complete; the backward alone is the
+    baseline, and the exposed time is what the step adds after it."""
+    import statistics
+    from paper_1805_07891_amd import workloads
+    from paper_1805_07891_amd.job import TorchJob
+    spec = wl.jobs[0]
+    N, K = spec.num_workers, spec.num_keys
+    key_group, ngroups = readiness_groups(spec, args.bucket_mb * 1e6)
+    prod_group, nprod = readiness_groups(spec, args.producer_mb * 1e6)
+    buckets = [[k for k in range(K) if prod_group[k] == b] for b in range(nprod)]
+    dim, mrows = 4096, 1024                       # one fixed GEMM shape for every bucket
+    flop_per_mm = 2.0 * mrows * dim * dim
+    n_mm = [max(1, int(round(args.backward_tflop * 1e12 * sum(spec.key_elems[k] for k in b)
+                             / spec.num_params / flop_per_mm))) for b in buckets]
+    weight = torch.randn(dim, dim, device=dev, dtype=torch.bfloat16)
+    acts = [torch.randn(mrows, dim, device=dev, dtype=torch.bfloat16) for _ in range(N)]
+    src = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, 0, 0, w) for w in range(N)]
+    w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, 0)
+    producers = [torch.cuda.Stream(device=dev) for _ in range(N)]
+    jobs = {}
+    for mode, kg in (("one_launch", None), ("groups", key_group)):
+        job = TorchJob(spec, dev, lib=lib, key_group=kg)
+        job.set_weights(w0)
+        arenas = [torch.zeros_like(src[w]) for w in range(N)]
+        for w in range(N):
+            job.attach_grads(w, arenas[w])
+        pushes = [[job.bucket(w, b) for b in buckets] for w in range(N)]
+        jobs[mode] = (job, arenas, pushes)
+    offs, arena_elems = workloads.key_offsets(spec.key_elems)
+    bounds = []
+    for b in buckets:
+        lo = offs[min(b)]
+        hi = offs[max(b) + 1] if max(b) + 1 < K else arena_elems
+        bounds.append((lo, hi))
+    torch.cuda.synchronize()
+
+    def backward(job, arenas, pushes):
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(producers[0])
+        for w in range(1, N):
+            producers[w].wait_event(start)
+        events = []
+        for bi in range(len(buckets)):
+            lo, hi = bounds[bi]
+            for w in range(N):
+                with torch.cuda.stream(producers[w]):
+                    for _ in range(n_mm[bi]):
+                        torch.mm(acts[w], weight)
+                    arenas[w][lo:hi].copy_(src[w][lo:hi])
+                    ev = torch.cuda.Event()
+                    ev.record(producers[w])
+                events.append(ev)
+                if pushes is not None:
+                    job.push_bucket(w, pushes[w][bi], ev)
+        return start, events
+
+    def run(mode, reps):
+        out = []
+        for _ in range(reps):
+            job, arenas, pushes = jobs["one_launch"] if mode == "backward_only" else jobs[mode]
+            start, events = backward(job, arenas, None if mode == "backward_only" else pushes)
+            end = torch.cuda.Event(enable_timing=True)
+            if mode == "backward_only":
+                for w in range(1, N):
+                    producers[0].wait_stream(producers[w])
+                end.record(producers[0])
+            else:
+                job.step()
+                end.record(job.stream)
+            torch.cuda.synchronize()
+            out.append(start.elapsed_time(end) * 1e3)
+        return out
+
+    print(f"streaming: {wl.name}, {N} workers, {len(buckets)} buckets per worker "
+          f"({sum(n_mm)} GEMMs of {mrows}x{dim}x{dim}), {ngroups} readiness groups",
+          file=sys.stderr, flush=True)
+    for mode in ("backward_only", "one_launch", "groups"):
+        print(f"streaming: warm-up {mode}", file=sys.stderr, flush=True)
+        run(mode, 3)
+    reps = max(5, args.steps // 25)
+    t = {m: [] for m in ("backward_only", "one_launch", "groups")}
+    for r in range(reps):                       # interleaved, so drift hits every mode
+        for m in t:
+            t[m] += run(m, 1)
+        print(f"streaming: rep {r + 1}/{reps}: " + ", ".join(f"{m} {v[-1]:.0f} us" for m, v in t.items()),
+              file=sys.stderr, flush=True)
+    med = {m: statistics.median(v) for m, v in t.items()}
+    out = {
+        "metric": "exchange time exposed after the backward pass (step end - backward end)",
+        "value": round(med["groups"] - med["backward_only"], 1),
+        "unit": "us",
+        "higher_is_better": False,
+        "n_gpus": 1,
+        "reps": reps,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "job": spec.name, "workers": N, "keys": K,
+                   "params": spec.num_params, "readiness_groups": ngroups,
+                   "bucket_mb": args.bucket_mb, "producer_buckets": nprod,
+                   "producer_mb": args.producer_mb, "gemm": [mrows, dim, dim],
+                   "bf16_tflop_per_worker": args.backward_tflop},
+        "median_us": {m: round(v, 1)
+                      for m, v in med.items()},
+        "min_us": {m: round(min(v), 1)
+                   for m, v in t.items()},
+        "exposed_us": {"one_launch": round(med["one_launch"] - med["backward_only"], 1),
+                       "groups": round(med["groups"] - med["backward_only"], 1)},
+    }
+    print(json.dumps(out), flush=True)
+    for job, _, _ in jobs.values():
+        job.destroy()
+    return 0
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -194,6 +332,16 @@ def main(argv=None) -> int:
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
+    ap.add_argument("--streaming", action="store_true",
+                    help="instead of the throughput line: time the step overlapped with a "
+                         "simulated backward pass, one launch vs readiness groups")
+    ap.add_argument("--bucket-mb", type=float, default=25.0,
+                    help="readiness group size for --streaming (MB of fp32 gradient per worker)")
+    ap.add_argument("--backward-tflop", type=float, default=1.0,
+                    help="--streaming: simulated backward work per worker (bf16 TFLOP)")
+    ap.add_argument("--producer-mb", type=float, default=8.0,
+                    help="--streaming: the simulated backward writes its gradients in buckets "
+                         "of this many MB per worker, one event each")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 512 MiB device copy three times (a known-size "
                          "reference for hardware byte counters)")
@@ -215,6 +363,9 @@ def main(argv=None) -> int:
     dev = torch.device("cuda:0")
     lib = load_library()
     wl = workloads.workload(args.workload)
+
+    if args.streaming:
+        return streaming_bench(torch, dev, lib, wl, args)
 
     if args.copy_calibration:
         src = torch.ones(128 << 20, dtype=torch.float32, device=dev)

@@ -169,10 +169,21 @@ int phub_push_event(phub_job *job, int worker, int key, const float *grad, void 
 /*
  * phub_push_keys - batched phub_push for one worker: pushes grads[i] for key
  * keys[i], i < count (keys == NULL means keys 0 .. count-1).  Same rules as
- * phub_push; either every pointer is recorded or, on error, none is.
+ * phub_push; either every pointer is recorded or, on an argument error,
+ * none is.
  */
 int phub_push_keys(phub_job *job, int worker, int count, const int *keys,
                    const float *const *grads);
+
+/*
+ * phub_push_keys_event - phub_push_keys whose gradients are all ready once
+ * `hip_event` has completed (as phub_push_event; NULL = ready now): one call
+ * per worker for a bucket of keys that one producer event covers.  Either
+ * every pointer is recorded or, on an argument error, none is; a group
+ * completed part-way through the call is enqueued at that point.
+ */
+int phub_push_keys_event(phub_job *job, int worker, int count, const int *keys,
+                         const float *const *grads, void *hip_event);
 
 /*
  * phub_step - aggregate and optimize every key (sections 3.2.2-3.2.4): one

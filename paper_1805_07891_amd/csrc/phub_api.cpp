@@ -635,6 +635,11 @@ int phub_push_event(phub_job* j, int worker, int key, const float* grad, void* h
 
 int phub_push_keys(phub_job* j, int worker, int count, const int* keys,
                    const float* const* grads) {
+    return phub_push_keys_event(j, worker, count, keys, grads, nullptr);
+}
+
+int phub_push_keys_event(phub_job* j, int worker, int count, const int* keys,
+                         const float* const* grads, void* hip_event) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     if (count < 0) return fail(PHUB_EINVAL, "count %d is negative", count);
     if (count > 0 && !grads) return fail(PHUB_EINVAL, "grads is NULL");
@@ -642,8 +647,9 @@ int phub_push_keys(phub_job* j, int worker, int count, const int* keys,
         return fail(PHUB_EINVAL, "count %d exceeds the %d keys", count, j->num_keys);
     for (int i = 0; i < count; ++i)
         if (int rc = check_grad(j, worker, keys ? keys[i] : i, grads[i])) return rc;
+    const hipEvent_t ev = static_cast<hipEvent_t>(hip_event);
     for (int i = 0; i < count; ++i)
-        if (int rc = record_push(j, worker, keys ? keys[i] : i, grads[i], nullptr)) return rc;
+        if (int rc = record_push(j, worker, keys ? keys[i] : i, grads[i], ev)) return rc;
     return PHUB_OK;
 }
 

@@ -115,6 +115,20 @@ class TorchJob:
         else:
             self.lib.phub_push_event(self.handle, worker, key, ptr, event.cuda_event)
 
+    def bucket(self, worker: int, keys: Sequence[int]):
+        """Prebuilt arguments for push_bucket: (key array, pointer array) of
+        ``keys`` in worker ``worker``'s attached arena."""
+        ptrs = self.key_pointers(self._grad_refs[worker])
+        return ((ctypes.c_int * len(keys))(*[int(k) for k in keys]),
+                _phub.pointer_array([ptrs[k] for k in keys]))
+
+    def push_bucket(self, worker: int, bucket, event=None) -> None:
+        """Push a prebuilt bucket (see ``bucket``) in one call, ready once
+        ``event`` (a torch.cuda.Event) has completed."""
+        keys, ptrs = bucket
+        self.lib.phub_push_keys_event(self.handle, worker, ptrs, keys,
+                                      None if event is None else event.cuda_event)
+
     def step(self) -> None:
         self.lib.phub_step(self.handle)
 

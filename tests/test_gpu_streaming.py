@@ -107,8 +107,8 @@ def test_groups_launched_as_they_complete_match_the_oracle(lib, torch_dev, group
     c.job.destroy()
 
 
-@pytest.mark.parametrize("grouped", [False, True])
-def test_ready_events_are_waited_on(lib, torch_dev, grouped):
+@pytest.mark.parametrize("grouped,batched", [(False, False), (True, False), (True, True)])
+def test_ready_events_are_waited_on(lib, torch_dev, grouped, batched):
     """Producers fill the gradient buffers on their own streams after a
     delay and record an event per key; the host pushes right away.  The step
     must read the produced values, not the zeros the buffers held."""
@@ -116,7 +116,7 @@ def test_ready_events_are_waited_on(lib, torch_dev, grouped):
     keys = (300000, 70001, 8193, 1024, 5)
     n_workers = 4
     key_group = list(range(len(keys))) if grouped else None
-    _say("ready events, grouped" if grouped else "ready events, one launch")
+    _say("ready events,", "grouped" if grouped else "one launch", "batched" if batched else "per key")
     c = Case(torch, dev, lib, n_workers, keys, key_group=key_group, seed=12)
     host = c.host_grads()
     src = [torch.from_numpy(a).to(dev) for a in host]
@@ -138,7 +138,10 @@ def test_ready_events_are_waited_on(lib, torch_dev, grouped):
                 ev = torch.cuda.Event()
                 ev.record(producers[w])
             events.append(ev)
-            c.job.push_key(w, k, ev)
+            if batched:
+                c.job.push_bucket(w, c.job.bucket(w, [k]), ev)
+            else:
+                c.job.push_key(w, k, ev)
     c.job.step()
     c.oracle_step(host)
     c.check("events")
