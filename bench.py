@@ -332,6 +332,9 @@ def main(argv=None) -> int:
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
+    ap.add_argument("--pushpull", action="store_true",
+                    help="every worker also receives the updated weights in its own model "
+                         "buffer, written by the same fused pass (PushPull)")
     ap.add_argument("--streaming", action="store_true",
                     help="instead of the throughput line: time the step overlapped with a "
                          "simulated backward pass, one launch vs readiness groups")
@@ -386,14 +389,24 @@ def main(argv=None) -> int:
         job.set_weights(w0)
         for w, a in enumerate(g):
             job.attach_grads(w, a)
+        if args.pushpull:
+            for w in range(spec.num_workers):
+                job.attach_models(w, torch.empty_like(w0))
         jobs.append(job)
         grads.append(g)
         w0s.append(w0)
     torch.cuda.synchronize()
 
+    def push(job):
+        if args.pushpull:
+            job.pushpull_all()
+        else:
+            job.push_all()
+
     for _ in range(args.warmup):
         for job in jobs:
-            job.push_and_step()
+            push(job)
+            job.step()
     torch.cuda.synchronize()
 
     K = args.steps
@@ -405,7 +418,7 @@ def main(argv=None) -> int:
     for s in range(K):
         h0 = time.perf_counter()
         for j, job in enumerate(jobs):
-            job.push_all()
+            push(job)
             ev[j][s][0].record(job.stream)
             job.step()
             ev[j][s][1].record(job.stream)
@@ -413,19 +426,23 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
+    def job_bytes(spec):
+        # the fused pass writes w' once more per worker with pushpull
+        return spec.hbm_bytes_per_step() + (spec.worker_grad_bytes_per_step() if args.pushpull else 0)
+
     ms_per_step = (t1 - t0) * 1e3 / K
     worker_bytes = wl.worker_grad_bytes_per_step()
     value = worker_bytes / (ms_per_step * 1e-3) / 1e9
-    whole_hbm = wl.hbm_bytes_per_step() / (ms_per_step * 1e-3) / 1e9
+    whole_hbm = sum(job_bytes(j) for j in wl.jobs) / (ms_per_step * 1e-3) / 1e9
 
     # dominant kernel: the job with the most bytes per launch
-    dom = max(range(len(jobs)), key=lambda j: wl.jobs[j].hbm_bytes_per_step())
+    dom = max(range(len(jobs)), key=lambda j: job_bytes(wl.jobs[j]))
     durs = sorted(ev[dom][s][0].elapsed_time(ev[dom][s][1]) for s in range(K))
     avg_ms = sum(durs) / len(durs)
     med_ms = durs[len(durs) // 2]
-    dom_bytes = wl.jobs[dom].hbm_bytes_per_step()
+    dom_bytes = job_bytes(wl.jobs[dom])
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.workload)
+    traffic = None if args.pushpull else measured_traffic(args.workload)
     groups, threads, segs, _ = jobs[dom].info()
     cache_resident = [job.info()[3] for job in jobs]
 
@@ -456,7 +473,8 @@ def main(argv=None) -> int:
             "chunk_bytes": wl.jobs[0].chunk_bytes,
             "optimizer": {"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
                           "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov},
-            "hbm_bytes_per_step": wl.hbm_bytes_per_step(),
+            "hbm_bytes_per_step": sum(job_bytes(j) for j in wl.jobs),
+            "pushpull": args.pushpull,
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},
             "host_us_per_step": round(host_s * 1e6 / K, 2),

@@ -186,6 +186,32 @@ int phub_push_keys_event(phub_job *job, int worker, int count, const int *keys,
                          const float *const *grads, void *hip_event);
 
 /*
+ * phub_pushpull - PushPull (section 3.1): push worker `worker`'s gradient
+ * for key `key` (as phub_push) and have the step write the key's updated
+ * weights into `model_out` (n_k fp32 values, 16-byte aligned, caller-owned;
+ * must not overlap any gradient, W, M or another model buffer).  The copy is
+ * written by the same fused pass that updates W, right after each piece of
+ * the key is optimized, so W is not read again to broadcast it.  The buffer
+ * is filled once the step has run on the job's stream (phub_sync, or an
+ * event recorded on the job's stream after phub_step).  The registration
+ * lasts for this step only.  In a step, or in a readiness group, either
+ * every (worker, key) pair gives a model buffer or none does: a mix is
+ * PHUB_EINVAL when the step (or the group) is enqueued, and nothing of it is
+ * enqueued.  Errors: as phub_push, and PHUB_EINVAL for a null or misaligned
+ * model_out.
+ */
+int phub_pushpull(phub_job *job, int worker, int key, const float *grad, float *model_out);
+
+/*
+ * phub_pushpull_keys - batched phub_pushpull for one worker, all gradients
+ * ready once `hip_event` has completed (NULL = ready now): grads[i] and
+ * model_outs[i] for key keys[i], i < count (keys == NULL means keys
+ * 0 .. count-1).  Argument errors are found before anything is recorded.
+ */
+int phub_pushpull_keys(phub_job *job, int worker, int count, const int *keys,
+                       const float *const *grads, float *const *model_outs, void *hip_event);
+
+/*
  * phub_step - aggregate and optimize every key (sections 3.2.2-3.2.4): one
  * kernel launch over all keys on the job's stream, asynchronous to the
  * host.  Requires every (worker, key) pair to have been pushed since the
@@ -198,7 +224,10 @@ int phub_push_keys_event(phub_job *job, int worker, int count, const int *keys,
  * PHUB_ENOTREADY (enqueuing nothing more) while a pair is missing: the groups
  * already enqueued stay applied, and the step completes once the missing
  * pushes arrive and phub_step is called again.
- * Errors: PHUB_ENOTREADY, PHUB_ESTATE, PHUB_EHIP.
+ * With pushpull registrations (phub_pushpull), the same pass also writes
+ * each key's updated weights into every worker's model buffer.
+ * Errors: PHUB_ENOTREADY, PHUB_EINVAL (a mix of pushes with and without a
+ * model buffer), PHUB_ESTATE, PHUB_EHIP.
  */
 int phub_step(phub_job *job);
 

@@ -105,6 +105,12 @@ __device__ __forceinline__ void store_wm(float* base, uint32_t byte_off, const f
         __builtin_nontemporal_store(v, a);
 }
 
+// Updated weights written to a worker's model buffer (pushpull): written
+// once and not read by the step, so non-temporal.
+__device__ __forceinline__ void store_out(float* base, uint32_t byte_off, const f4& v) {
+    __builtin_nontemporal_store(v, (PHUB_GLOBAL f4*)((PHUB_GLOBAL char*)base + byte_off));
+}
+
 __device__ __forceinline__ float load1(const float* base, int64_t i) {
     return ((const PHUB_GLOBAL float*)base)[i];
 }
@@ -123,8 +129,9 @@ __device__ __forceinline__ uint32_t wave_index() {
 #define PHUB_KERNEL_ARGS                                                                  \
     const DevTile* __restrict__ tiles, const int32_t* __restrict__ tile_begin,            \
         const DevRem* __restrict__ rems, const int32_t* __restrict__ rem_begin,           \
-        const float* const* __restrict__ grads, float* __restrict__ weights,              \
-        float* __restrict__ moments, float lr, float mu, float wd, int num_workers
+        const float* const* __restrict__ grads, float* const* __restrict__ outs,          \
+        float* __restrict__ weights, float* __restrict__ moments, float lr, float mu,     \
+        float wd, int num_workers
 
 // Splits a tile's float4 index into a part folded into the base pointers
 // (a multiple of 2^20 float4, 16 MB) and a low part that keeps the per-lane
@@ -142,6 +149,7 @@ struct TileStreams {
     float* w;
     float* m;
     uint32_t off;
+    uint32_t vhi;  // float4 index folded into the gradient (and output) bases
 };
 
 template <int NW>
@@ -161,6 +169,7 @@ __device__ __forceinline__ void tile_streams(TileStreams<NW>& s, const DevTile& 
     const uint32_t vhi = uint32_t(d.vec) & ~kVecLowMask;
 #pragma unroll
     for (int w = 0; w < NW; ++w) s.g[w] = row[w] + size_t(vhi) * 4;
+    s.vhi = vhi;
     tile_bases<NW>(s, d, weights, moments);
 }
 
@@ -188,6 +197,7 @@ __device__ __forceinline__ void tile_streams(TileStreams<NW>& s, const DevTile& 
     const uint32_t vhi = uint32_t(d.vec) & ~kVecLowMask;
 #pragma unroll
     for (int w = 0; w < NW; ++w) s.g[w] = lane_pointer(row, w) + size_t(vhi) * 4;
+    s.vhi = vhi;
     tile_bases<NW>(s, d, weights, moments);
 }
 
@@ -244,10 +254,10 @@ struct TilePipe {
 // first load of the next tile is issued, the next tile's streams are formed
 // from its descriptor and pointer row, which were fetched at the start of
 // this tile.
-template <int NW, bool NEST, bool RES, int I>
+template <int NW, bool NEST, bool RES, bool PULL, int I>
 __device__ __forceinline__ void tile_step(TilePipe<NW, RES>& p, const TileStreams<NW>& a,
                                           TileStreams<NW>& b, const DevTile& nd,
-                                          uint64_t nrow, bool has_next,
+                                          uint64_t nrow, uint64_t prow, bool has_next,
                                           float* weights, float* moments, float nlr, float mu,
                                           float wd) {
     constexpr int L = kTileLoads<NW>;
@@ -279,17 +289,25 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, RES>& p, const TileStream
         optimize4<NEST>(p.acc[u], p.wv[u], p.mv[u], nlr, mu, wd);
         store_wm<RES>(a.w, a.off + u * 1024u, p.wv[u]);
         store_wm<RES>(a.m, a.off + u * 1024u, p.mv[u]);
+        if constexpr (PULL) {
+            // the piece of w' into every worker's model buffer (pushpull)
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+                store_out(const_cast<float*>(lane_pointer(prow, w)) + size_t(a.vhi) * 4,
+                          a.off + u * 1024u, p.wv[u]);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int NW, bool NEST, bool RES, int... I>
+template <int NW, bool NEST, bool RES, bool PULL, int... I>
 __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>, TilePipe<NW, RES>& p,
                                            const TileStreams<NW>& a, TileStreams<NW>& b,
-                                           const DevTile& nd, uint64_t nrow,
+                                           const DevTile& nd, uint64_t nrow, uint64_t prow,
                                            bool has_next, float* weights, float* moments,
                                            float nlr, float mu, float wd) {
-    (tile_step<NW, NEST, RES, I>(p, a, b, nd, nrow, has_next, weights, moments, nlr, mu, wd),
+    (tile_step<NW, NEST, RES, PULL, I>(p, a, b, nd, nrow, prow, has_next, weights, moments, nlr,
+                                       mu, wd),
      ...);
 }
 
@@ -301,10 +319,10 @@ __device__ __forceinline__ void tile_prologue(std::integer_sequence<int, I...>, 
 
 // The rest of a segment: nvec < 256 float4 then a ragged end of rem < 4
 // elements (one per lane).
-template <int NW, bool NEST, bool RES>
+template <int NW, bool NEST, bool RES, bool PULL>
 __device__ __forceinline__ void partial(const float* const* g, float* wb, float* mb,
-                                        uint32_t nvec, uint32_t rem, float nlr, float mu,
-                                        float wd) {
+                                        float* const* out, uint32_t nvec, uint32_t rem,
+                                        float nlr, float mu, float wd) {
     const uint32_t lane = threadIdx.x & 63u;
     for (uint32_t v = lane; v < nvec; v += 64u) {
         f4 a[NW];
@@ -318,6 +336,10 @@ __device__ __forceinline__ void partial(const float* const* g, float* wb, float*
         optimize4<NEST>(s, wv, mv, nlr, mu, wd);
         store_wm<RES>(wb, v * 16u, wv);
         store_wm<RES>(mb, v * 16u, mv);
+        if constexpr (PULL) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) store_out(out[w], v * 16u, wv);
+        }
     }
     if (lane < rem) {
         const int64_t i = int64_t(nvec) * 4 + lane;
@@ -328,6 +350,10 @@ __device__ __forceinline__ void partial(const float* const* g, float* wb, float*
         optimize<NEST>(s, wv, mv, nlr, mu, wd);
         store1(wb, i, wv);
         store1(mb, i, mv);
+        if constexpr (PULL) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) store1(out[w], i, wv);
+        }
     }
 }
 
@@ -341,7 +367,7 @@ __device__ __forceinline__ void partial(const float* const* g, float* wb, float*
 // One wave per SIMD (one workgroup of 4 waves per CU).
 #define PHUB_ONE_WAVE_PER_SIMD __attribute__((amdgpu_waves_per_eu(1, 1)))
 
-template <int NW, bool NEST, bool RES>
+template <int NW, bool NEST, bool RES, bool PULL>
 __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_step_fixed(
     PHUB_KERNEL_ARGS) {
     static_assert(kTileLoads<NW> % kRing<NW, RES> == 0, "the load window must wrap with the tile");
@@ -354,21 +380,27 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
         const int32_t last = te - 1;
         TilePipe<NW, RES> p;
         TileStreams<NW> a, b;
+        uint64_t prow = 0;  // pushpull: model-buffer pointer row of the current tile
         {
             const DevTile first = tiles[tb];
             tile_streams<NW>(a, first, grads + int64_t(first.key) * NW, weights, moments);
+            if constexpr (PULL) prow = load_row<NW>(outs + int64_t(first.key) * NW);
         }
         DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
         tile_prologue<NW, RES>(std::make_integer_sequence<int, kAhead<NW, RES>>{}, p, a);
         for (int32_t t = tb;; ++t) {
             const bool has_next = t < last;
             const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
+            uint64_t nprow = 0;
+            if constexpr (PULL) nprow = load_row<NW>(outs + int64_t(nd.key) * NW);
             const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
-            tile_steps<NW, NEST, RES>(std::make_integer_sequence<int, kTileLoads<NW>>{}, p, a, b,
-                                      nd, nrow, has_next, weights, moments, nlr, mu, wd);
+            tile_steps<NW, NEST, RES, PULL>(std::make_integer_sequence<int, kTileLoads<NW>>{}, p,
+                                            a, b, nd, nrow, prow, has_next, weights, moments, nlr,
+                                            mu, wd);
             if (!has_next) break;
             a = b;
             nd = nd2;
+            prow = nprow;
         }
     }
 
@@ -377,10 +409,15 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
     for (int32_t r = rb; r < re; ++r) {
         const DevRem rm = rems[r];
         const float* g[NW];
+        float* out[NW];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) g[w] = grads[int64_t(rm.key) * NW + w] + rm.offset;
-        partial<NW, NEST, RES>(g, weights + rm.arena_offset, moments + rm.arena_offset,
-                               uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u, nlr, mu, wd);
+        for (int w = 0; w < NW; ++w) {
+            g[w] = grads[int64_t(rm.key) * NW + w] + rm.offset;
+            out[w] = PULL ? outs[int64_t(rm.key) * NW + w] + rm.offset : nullptr;
+        }
+        partial<NW, NEST, RES, PULL>(g, weights + rm.arena_offset, moments + rm.arena_offset, out,
+                                     uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u, nlr, mu,
+                                     wd);
     }
 }
 
@@ -388,10 +425,10 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
 // together, the running sum carried across batches in worker order.
 constexpr int kBatch = 8;
 
-template <bool NEST, bool RES>
-__device__ __forceinline__ void run_any(const float* const* kp, int n, int64_t offset, float* wb,
-                                        float* mb, uint32_t nvec, uint32_t rem, float nlr,
-                                        float mu, float wd) {
+template <bool NEST, bool RES, bool PULL>
+__device__ __forceinline__ void run_any(const float* const* kp, float* const* ko, int n,
+                                        int64_t offset, float* wb, float* mb, uint32_t nvec,
+                                        uint32_t rem, float nlr, float mu, float wd) {
     const uint32_t lane = threadIdx.x & 63u;
     for (uint32_t v = lane; v < nvec; v += 64u) {
         const uint32_t bo = v * 16u;
@@ -410,6 +447,8 @@ __device__ __forceinline__ void run_any(const float* const* kp, int n, int64_t o
         optimize4<NEST>(s, wv, mv, nlr, mu, wd);
         store_wm<RES>(wb, bo, wv);
         store_wm<RES>(mb, bo, mv);
+        if constexpr (PULL)
+            for (int w = 0; w < n; ++w) store_out(ko[w] + offset, bo, wv);
     }
     if (lane < rem) {
         const int64_t i = int64_t(nvec) * 4 + lane;
@@ -419,10 +458,12 @@ __device__ __forceinline__ void run_any(const float* const* kp, int n, int64_t o
         optimize<NEST>(s, wv, mv, nlr, mu, wd);
         store1(wb, i, wv);
         store1(mb, i, mv);
+        if constexpr (PULL)
+            for (int w = 0; w < n; ++w) store1(ko[w] + offset, i, wv);
     }
 }
 
-template <bool NEST, bool RES>
+template <bool NEST, bool RES, bool PULL>
 __global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS) {
     const uint32_t wave = wave_index();
     const int n = num_workers;
@@ -431,42 +472,52 @@ __global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS
     const int32_t te = tile_begin[wave + 1];
     for (int32_t t = tb; t < te; ++t) {
         const DevTile tl = tiles[t];
-        run_any<NEST, RES>(grads + int64_t(tl.key) * n, n, int64_t(tl.vec) * 4,
-                           weights + tl.arena_offset, moments + tl.arena_offset,
-                           uint32_t(kTileElems / 4), 0u, nlr, mu, wd);
+        run_any<NEST, RES, PULL>(grads + int64_t(tl.key) * n, PULL ? outs + int64_t(tl.key) * n : nullptr,
+                                 n, int64_t(tl.vec) * 4, weights + tl.arena_offset,
+                                 moments + tl.arena_offset, uint32_t(kTileElems / 4), 0u, nlr, mu,
+                                 wd);
     }
     const int32_t rb = rem_begin[wave];
     const int32_t re = rem_begin[wave + 1];
     for (int32_t r = rb; r < re; ++r) {
         const DevRem rm = rems[r];
-        run_any<NEST, RES>(grads + int64_t(rm.key) * n, n, rm.offset, weights + rm.arena_offset,
-                           moments + rm.arena_offset, uint32_t(rm.count) >> 2,
-                           uint32_t(rm.count) & 3u, nlr, mu, wd);
+        run_any<NEST, RES, PULL>(grads + int64_t(rm.key) * n, PULL ? outs + int64_t(rm.key) * n : nullptr,
+                                 n, rm.offset, weights + rm.arena_offset,
+                                 moments + rm.arena_offset, uint32_t(rm.count) >> 2,
+                                 uint32_t(rm.count) & 3u, nlr, mu, wd);
     }
 }
 
 #define PHUB_LAUNCH_ARGS                                                                    \
-    p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.weights, p.moments, p.lr, p.mu, \
-        p.wd, p.num_workers
+    p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.outs, p.weights, p.moments, p.lr, \
+        p.mu, p.wd, p.num_workers
+
+template <bool NEST, bool RES, bool PULL>
+hipError_t launch_any(const StepParams& p, int grid, hipStream_t stream) {
+    hipLaunchKernelGGL((fused_step_any<NEST, RES, PULL>), dim3(grid), dim3(kBlockThreads), 0,
+                       stream, PHUB_LAUNCH_ARGS);
+    return hipGetLastError();
+}
+
+template <int NW, bool NEST, bool RES, bool PULL>
+hipError_t launch_one(const StepParams& p, int grid, hipStream_t stream) {
+    if constexpr (kTileLoads<NW> % kRing<NW, RES> == 0) {
+        hipLaunchKernelGGL((fused_step_fixed<NW, NEST, RES, PULL>), dim3(grid),
+                           dim3(kBlockThreads), 0, stream, PHUB_LAUNCH_ARGS);
+        return hipGetLastError();
+    } else {
+        return launch_any<NEST, RES, PULL>(p, grid, stream);
+    }
+}
 
 template <int NW, bool RES>
 hipError_t launch_n(const StepParams& p, bool nesterov, int grid, hipStream_t stream) {
-    if constexpr (kTileLoads<NW> % kRing<NW, RES> == 0) {
-        if (nesterov)
-            hipLaunchKernelGGL((fused_step_fixed<NW, true, RES>), dim3(grid), dim3(kBlockThreads),
-                               0, stream, PHUB_LAUNCH_ARGS);
-        else
-            hipLaunchKernelGGL((fused_step_fixed<NW, false, RES>), dim3(grid),
-                               dim3(kBlockThreads), 0, stream, PHUB_LAUNCH_ARGS);
-    } else {
-        if (nesterov)
-            hipLaunchKernelGGL((fused_step_any<true, RES>), dim3(grid), dim3(kBlockThreads), 0,
-                               stream, PHUB_LAUNCH_ARGS);
-        else
-            hipLaunchKernelGGL((fused_step_any<false, RES>), dim3(grid), dim3(kBlockThreads), 0,
-                               stream, PHUB_LAUNCH_ARGS);
-    }
-    return hipGetLastError();
+    const bool pull = p.outs != nullptr;
+    if (nesterov)
+        return pull ? launch_one<NW, true, RES, true>(p, grid, stream)
+                    : launch_one<NW, true, RES, false>(p, grid, stream);
+    return pull ? launch_one<NW, false, RES, true>(p, grid, stream)
+                : launch_one<NW, false, RES, false>(p, grid, stream);
 }
 
 template <bool RES>
@@ -488,14 +539,14 @@ hipError_t launch_res(const StepParams& p, bool nesterov, int grid, hipStream_t 
         case 14: return launch_n<14, RES>(p, nesterov, grid, stream);
         case 15: return launch_n<15, RES>(p, nesterov, grid, stream);
         case 16: return launch_n<16, RES>(p, nesterov, grid, stream);
-        default:
+        default: {
+            const bool pull = p.outs != nullptr;
             if (nesterov)
-                hipLaunchKernelGGL((fused_step_any<true, RES>), dim3(grid), dim3(kBlockThreads), 0,
-                                   stream, PHUB_LAUNCH_ARGS);
-            else
-                hipLaunchKernelGGL((fused_step_any<false, RES>), dim3(grid), dim3(kBlockThreads), 0,
-                                   stream, PHUB_LAUNCH_ARGS);
-            return hipGetLastError();
+                return pull ? launch_any<true, RES, true>(p, grid, stream)
+                            : launch_any<true, RES, false>(p, grid, stream);
+            return pull ? launch_any<false, RES, true>(p, grid, stream)
+                        : launch_any<false, RES, false>(p, grid, stream);
+        }
     }
 }
 

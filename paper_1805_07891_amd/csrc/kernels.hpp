@@ -49,6 +49,7 @@ struct StepParams {
     const DevRem* rems;           // grouped by bin
     const int32_t* rem_begin;     // wave w owns rems [rem_begin[w], rem_begin[w+1])
     const float* const* grads;    // [row * num_workers + worker], 16-byte aligned
+    float* const* outs;           // same layout: model buffers that receive w' (pushpull), or null
     float* weights;               // W arena
     float* moments;               // M arena
     float lr;
@@ -57,7 +58,9 @@ struct StepParams {
     int num_workers;
 };
 
-// Enqueues one fused aggregate + optimize pass over the whole schedule:
+// Enqueues one fused aggregate + optimize pass over the whole schedule
+// (and, when p.outs is set, writes the updated weights into every worker's
+// model buffer in the same pass):
 // `grid` workgroups of kBlockThreads threads, one bin per wave (the bin
 // tables have grid * kBlockThreads / 64 + 1 entries).  `resident`: W and M
 // use the cache-allocating policy instead of non-temporal accesses.

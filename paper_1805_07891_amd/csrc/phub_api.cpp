@@ -122,6 +122,8 @@ struct phub_job {
     std::vector<int64_t> rgroup_pushed;  // (worker, key) pairs pushed this step
     std::vector<uint8_t> rgroup_launched;
     std::vector<uint8_t> rgroup_dirty;   // its rows changed since they were last uploaded
+    std::vector<int64_t> rgroup_outs;    // pushpull: model buffers registered this step
+    std::vector<uint8_t> rgroup_out_dirty;
 
     float* weights = nullptr;
     float* moments = nullptr;
@@ -130,15 +132,19 @@ struct phub_job {
     phub::DevRem* d_rems = nullptr;
     int32_t* d_rem_begin = nullptr;   // same layout
     const float** d_grads = nullptr;  // [row * N + worker]
+    float** d_outs = nullptr;         // same layout: pushpull model buffers
 
     std::vector<const float*> grads;  // host table, [row * N + worker]
     std::vector<hipEvent_t> ready;    // same layout: event to wait for (none if null)
     std::vector<uint8_t> pushed;      // same layout: pushed since the last step
     int64_t num_pushed = 0;
+    std::vector<float*> outs;         // same layout: pushpull model buffers of this step
+    std::vector<uint8_t> has_out;
 
     // Pinned staging of the pointer table: one slot per step, reused after
     // kStageSlots steps once the copies that read it have run.
     const float** stage[kStageSlots] = {};
+    float** stage_out[kStageSlots] = {};
     hipEvent_t stage_done[kStageSlots] = {};
     bool stage_used[kStageSlots] = {};
     int stage_slot = 0;
@@ -172,6 +178,7 @@ bool is_live(const phub_job* j) {
 
 void release(phub_job* j) {
     if (j->d_grads) (void)hipFree(j->d_grads);
+    if (j->d_outs) (void)hipFree(j->d_outs);
     if (j->d_tile_begin) (void)hipFree(j->d_tile_begin);
     if (j->d_tiles) (void)hipFree(j->d_tiles);
     if (j->d_rem_begin) (void)hipFree(j->d_rem_begin);
@@ -181,6 +188,7 @@ void release(phub_job* j) {
     for (int i = 0; i < kStageSlots; ++i) {
         if (j->stage_done[i]) (void)hipEventDestroy(j->stage_done[i]);
         if (j->stage[i]) (void)hipHostFree(j->stage[i]);
+        if (j->stage_out[i]) (void)hipHostFree(j->stage_out[i]);
     }
     if (j->own_stream && j->stream) (void)hipStreamDestroy(j->stream);
     delete j;
@@ -208,9 +216,9 @@ int check_grad(const phub_job* j, int worker, int key, const float* grad) {
     return PHUB_OK;
 }
 
-// Copies the rows of group g from the host table to the device, through the
-// current step's pinned staging slot, on the job's stream.
-int upload_rows(phub_job* j, int g) {
+// Claims the current step's pinned staging slot: waits until the copies
+// that last read it (kStageSlots steps ago) have run.
+int claim_stage(phub_job* j) {
     const int slot = j->stage_slot;
     if (!j->stage_claimed) {
         if (j->stage_used[slot]) {
@@ -219,20 +227,46 @@ int upload_rows(phub_job* j, int g) {
         }
         j->stage_claimed = true;
     }
-    const size_t n = size_t(j->num_workers);
-    const size_t r0 = size_t(j->rgroup_row_begin[g]) * n;
-    const size_t r1 = size_t(j->rgroup_row_begin[g + 1]) * n;
+    return PHUB_OK;
+}
+
+// Copies rows [r0, r1) of a host pointer table to the device, through the
+// current step's staging slot, on the job's stream.
+template <typename T>
+int upload_range(phub_job* j, T* const* host, T** stage, T** dev, size_t r0, size_t r1) {
+    if (int rc = claim_stage(j)) return rc;
     if (r1 > r0) {
-        std::memcpy(j->stage[slot] + r0, j->grads.data() + r0, (r1 - r0) * sizeof(const float*));
-        hipError_t e = hipMemcpyAsync(j->d_grads + r0, j->stage[slot] + r0,
-                                      (r1 - r0) * sizeof(const float*), hipMemcpyHostToDevice,
-                                      j->stream);
+        const int slot = j->stage_slot;
+        std::memcpy(stage + r0, host + r0, (r1 - r0) * sizeof(T*));
+        hipError_t e = hipMemcpyAsync(dev + r0, stage + r0, (r1 - r0) * sizeof(T*),
+                                      hipMemcpyHostToDevice, j->stream);
         if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pointer table)");
         e = hipEventRecord(j->stage_done[slot], j->stream);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord (pointer staging)");
         j->stage_used[slot] = true;
     }
+    return PHUB_OK;
+}
+
+// The gradient rows of group g.
+int upload_rows(phub_job* j, int g) {
+    const size_t n = size_t(j->num_workers);
+    if (int rc = upload_range<const float>(j, j->grads.data(), j->stage[j->stage_slot], j->d_grads,
+                                           size_t(j->rgroup_row_begin[g]) * n,
+                                           size_t(j->rgroup_row_begin[g + 1]) * n))
+        return rc;
     j->rgroup_dirty[g] = 0;
+    return PHUB_OK;
+}
+
+// The model-buffer rows of group g (pushpull).
+int upload_out_rows(phub_job* j, int g) {
+    const size_t n = size_t(j->num_workers);
+    if (int rc = upload_range<float>(j, j->outs.data(), j->stage_out[j->stage_slot], j->d_outs,
+                                     size_t(j->rgroup_row_begin[g]) * n,
+                                     size_t(j->rgroup_row_begin[g + 1]) * n))
+        return rc;
+    j->rgroup_out_dirty[g] = 0;
     return PHUB_OK;
 }
 
@@ -240,11 +274,23 @@ int upload_rows(phub_job* j, int g) {
 // distinct ready event of its pushes, then the fused kernel over its
 // schedule.
 int launch_group(phub_job* j, int g) {
+    const size_t n = size_t(j->num_workers);
+    const int64_t pairs = int64_t(j->rgroup_row_begin[g + 1] - j->rgroup_row_begin[g]) * j->num_workers;
+    const bool pull = j->rgroup_outs[g] > 0;
+    if (pull && j->rgroup_outs[g] != pairs) {
+        for (size_t i = size_t(j->rgroup_row_begin[g]) * n; i < size_t(j->rgroup_row_begin[g + 1]) * n; ++i)
+            if (!j->has_out[i])
+                return fail(PHUB_EINVAL,
+                            "pushpull: worker %d gave no model buffer for key %d while other "
+                            "pushes of its readiness group did",
+                            int(i % n), j->key_of_row[i / n]);
+    }
     DeviceScope ds(j->device);
     if (!ds.ok()) return fail(PHUB_EHIP, "cannot make device %d current", j->device);
     if (j->rgroup_dirty[g])
         if (int rc = upload_rows(j, g)) return rc;
-    const size_t n = size_t(j->num_workers);
+    if (pull && j->rgroup_out_dirty[g])
+        if (int rc = upload_out_rows(j, g)) return rc;
     std::vector<hipEvent_t> evs;
     for (size_t i = size_t(j->rgroup_row_begin[g]) * n; i < size_t(j->rgroup_row_begin[g + 1]) * n;
          ++i)
@@ -262,6 +308,7 @@ int launch_group(phub_job* j, int g) {
         p.rems = j->d_rems;
         p.rem_begin = j->d_rem_begin + size_t(g) * (j->bins + 1);
         p.grads = j->d_grads;
+        p.outs = pull ? j->d_outs : nullptr;
         p.weights = j->weights;
         p.moments = j->moments;
         p.lr = j->lr;
@@ -272,6 +319,29 @@ int launch_group(phub_job* j, int g) {
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
     }
     j->rgroup_launched[g] = 1;
+    return PHUB_OK;
+}
+
+// Registers worker `worker`'s model buffer for key `key` in this step.
+void record_out(phub_job* j, int worker, int key, float* out) {
+    const int g = j->key_rgroup[key];
+    const size_t i = size_t(j->row_of_key[key]) * j->num_workers + worker;
+    if (j->outs[i] != out) {
+        j->outs[i] = out;
+        j->rgroup_out_dirty[g] = 1;
+    }
+    if (!j->has_out[i]) {
+        j->has_out[i] = 1;
+        ++j->rgroup_outs[g];
+    }
+}
+
+int check_out(const phub_job* j, int worker, int key, const float* out) {
+    if (!out && j->key_elems[key] != 0)
+        return fail(PHUB_EINVAL, "model buffer of worker %d for key %d is NULL", worker, key);
+    if (reinterpret_cast<uintptr_t>(out) % 16 != 0)
+        return fail(PHUB_EINVAL, "model buffer of worker %d for key %d is not 16-byte aligned",
+                    worker, key);
     return PHUB_OK;
 }
 
@@ -404,6 +474,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->grads.assign(size_t(num_workers) * num_keys, nullptr);
         j->ready.assign(size_t(num_workers) * num_keys, nullptr);
         j->pushed.assign(size_t(num_workers) * num_keys, 0);
+        j->outs.assign(size_t(num_workers) * num_keys, nullptr);
+        j->has_out.assign(size_t(num_workers) * num_keys, 0);
         // readiness groups; rows of the pointer table ordered by group, then key
         j->streaming = num_rgroups > 0;
         j->num_rgroups = j->streaming ? num_rgroups : 1;
@@ -424,6 +496,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->rgroup_pushed.assign(j->num_rgroups, 0);
         j->rgroup_launched.assign(j->num_rgroups, 0);
         j->rgroup_dirty.assign(j->num_rgroups, 1);
+        j->rgroup_outs.assign(j->num_rgroups, 0);
+        j->rgroup_out_dirty.assign(j->num_rgroups, 1);
     } catch (const std::bad_alloc&) {
         delete j;
         return fail(PHUB_ENOMEM, "host allocation of the job tables failed");
@@ -555,7 +629,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             hipMalloc(&j->d_tile_begin, tb_bytes) != hipSuccess ||
             hipMalloc(&j->d_rems, rem_bytes) != hipSuccess ||
             hipMalloc(&j->d_rem_begin, rb_bytes) != hipSuccess ||
-            hipMalloc(&j->d_grads, tab_bytes) != hipSuccess) {
+            hipMalloc(&j->d_grads, tab_bytes) != hipSuccess ||
+            hipMalloc(&j->d_outs, tab_bytes) != hipSuccess) {
             (void)hipGetLastError();
             rc = fail(PHUB_ENOMEM, "device allocation of the schedule failed");
             goto fail_cleanup;
@@ -574,6 +649,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                  "hipMemcpy(remainder bins)");
         for (int i = 0; i < kStageSlots; ++i) {
             if (hipHostMalloc(reinterpret_cast<void**>(&j->stage[i]), tab_bytes,
+                              hipHostMallocDefault) != hipSuccess ||
+                hipHostMalloc(reinterpret_cast<void**>(&j->stage_out[i]), tab_bytes,
                               hipHostMallocDefault) != hipSuccess) {
                 (void)hipGetLastError();
                 rc = fail(PHUB_ENOMEM, "pinned host allocation of the pointer staging failed");
@@ -633,6 +710,35 @@ int phub_push_event(phub_job* j, int worker, int key, const float* grad, void* h
     return record_push(j, worker, key, grad, static_cast<hipEvent_t>(hip_event));
 }
 
+int phub_pushpull(phub_job* j, int worker, int key, const float* grad, float* model_out) {
+    return phub_pushpull_keys(j, worker, 1, &key, &grad, &model_out, nullptr);
+}
+
+int phub_pushpull_keys(phub_job* j, int worker, int count, const int* keys,
+                       const float* const* grads, float* const* model_outs, void* hip_event) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (count < 0) return fail(PHUB_EINVAL, "count %d is negative", count);
+    if (count > 0 && (!grads || !model_outs)) return fail(PHUB_EINVAL, "grads or model_outs is NULL");
+    if (!keys && count > j->num_keys)
+        return fail(PHUB_EINVAL, "count %d exceeds the %d keys", count, j->num_keys);
+    for (int i = 0; i < count; ++i) {
+        const int key = keys ? keys[i] : i;
+        if (int rc = check_grad(j, worker, key, grads[i])) return rc;
+        if (int rc = check_out(j, worker, key, model_outs[i])) return rc;
+    }
+    const hipEvent_t ev = static_cast<hipEvent_t>(hip_event);
+    for (int i = 0; i < count; ++i) {
+        const int key = keys ? keys[i] : i;
+        if (j->streaming && j->rgroup_launched[j->key_rgroup[key]])
+            return fail(PHUB_ESTATE,
+                        "key %d belongs to readiness group %d, which was already launched this "
+                        "step", key, j->key_rgroup[key]);
+        record_out(j, worker, key, model_outs[i]);  // before the push that may launch the group
+        if (int rc = record_push(j, worker, key, grads[i], ev)) return rc;
+    }
+    return PHUB_OK;
+}
+
 int phub_push_keys(phub_job* j, int worker, int count, const int* keys,
                    const float* const* grads) {
     return phub_push_keys_event(j, worker, count, keys, grads, nullptr);
@@ -672,6 +778,8 @@ int phub_step(phub_job* j) {
     std::fill(j->ready.begin(), j->ready.end(), nullptr);
     std::fill(j->rgroup_pushed.begin(), j->rgroup_pushed.end(), 0);
     std::fill(j->rgroup_launched.begin(), j->rgroup_launched.end(), 0);
+    std::fill(j->has_out.begin(), j->has_out.end(), 0);
+    std::fill(j->rgroup_outs.begin(), j->rgroup_outs.end(), 0);
     j->num_pushed = 0;
     if (j->stage_claimed) {
         j->stage_slot = (j->stage_slot + 1) % kStageSlots;

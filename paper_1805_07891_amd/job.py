@@ -129,6 +129,23 @@ class TorchJob:
         self.lib.phub_push_keys_event(self.handle, worker, ptrs, keys,
                                       None if event is None else event.cuda_event)
 
+    def attach_models(self, worker: int, arena) -> None:
+        """Use ``arena`` (arena_elems fp32 values) as worker ``worker``'s model
+        buffer for pushpull: every key's updated weights land at its offset."""
+        if arena.numel() != self.arena_elems or arena.dtype != self.torch.float32:
+            raise ValueError("model arena has the wrong size or dtype")
+        if not hasattr(self, "_model_refs"):
+            self._model_refs = [None] * self.spec.num_workers
+            self._model_ptrs = [None] * self.spec.num_workers
+        self._model_refs[worker] = arena
+        self._model_ptrs[worker] = _phub.pointer_array(self.key_pointers(arena))
+
+    def pushpull_all(self) -> None:
+        """Every worker pushes all its keys and asks for the updated weights
+        in its attached model buffer."""
+        for w, arr in enumerate(self._ptr_arrays):
+            self.lib.phub_pushpull_keys(self.handle, w, arr, self._model_ptrs[w])
+
     def step(self) -> None:
         self.lib.phub_step(self.handle)
 

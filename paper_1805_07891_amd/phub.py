@@ -32,7 +32,7 @@ PHUB_SCHEDULE_LPT = 1
 
 # Every symbol the header declares.
 EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_push_event",
-            "phub_push_keys", "phub_push_keys_event",
+            "phub_push_keys", "phub_push_keys_event", "phub_pushpull", "phub_pushpull_keys",
             "phub_step", "phub_pull", "phub_get_state", "phub_sync", "phub_get_stream",
             "phub_job_info", "phub_destroy", "phub_last_error", "phub_plan_count",
             "phub_plan_build")
@@ -72,6 +72,8 @@ class Library:
             "phub_push_event": ([vp, i32, i32, vp, vp], i32),
             "phub_push_keys": ([vp, i32, i32, vp, vp], i32),
             "phub_push_keys_event": ([vp, i32, i32, vp, vp, vp], i32),
+            "phub_pushpull": ([vp, i32, i32, vp, vp], i32),
+            "phub_pushpull_keys": ([vp, i32, i32, vp, vp, vp, vp], i32),
             "phub_step": ([vp], i32),
             "phub_pull": ([vp, i32, pp], i32),
             "phub_get_state": ([vp, i32, pp, pp], i32),
@@ -154,6 +156,23 @@ class Library:
             karr = (ctypes.c_int * len(keys))(*[int(k) for k in keys])
         return self._check(self.lib.phub_push_keys(job, int(worker), len(grad_ptrs),
                                                    karr, grad_ptrs), check)
+
+    def phub_pushpull(self, job, worker: int, key: int, grad_ptr: int, out_ptr: int,
+                      check: bool = True) -> int:
+        return self._check(self.lib.phub_pushpull(job, int(worker), int(key), grad_ptr, out_ptr),
+                           check)
+
+    def phub_pushpull_keys(self, job, worker: int, grad_ptrs, out_ptrs, keys=None,
+                           hip_event: Optional[int] = None, check: bool = True) -> int:
+        if not isinstance(grad_ptrs, ctypes.Array):
+            grad_ptrs = pointer_array(grad_ptrs)
+        if not isinstance(out_ptrs, ctypes.Array):
+            out_ptrs = pointer_array(out_ptrs)
+        karr = keys
+        if keys is not None and not isinstance(keys, ctypes.Array):
+            karr = (ctypes.c_int * len(keys))(*[int(k) for k in keys])
+        return self._check(self.lib.phub_pushpull_keys(job, int(worker), len(grad_ptrs), karr,
+                                                       grad_ptrs, out_ptrs, hip_event), check)
 
     def phub_push_keys_event(self, job, worker: int, grad_ptrs, keys, hip_event: Optional[int],
                              check: bool = True) -> int:
