@@ -329,12 +329,20 @@ def main(argv=None) -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of the CPU oracle baseline (0 skips it)")
+    ap.add_argument("--chunk-bytes", type=int, default=None,
+                    help="chunk size of the schedule (default: the workload's, 32 KB)")
+    ap.add_argument("--schedule", choices=("lpt", "split"), default="lpt",
+                    help="chunk-to-wave schedule: the paper's balanced partition (lpt) or "
+                         "contiguous, exactly balanced runs (split)")
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
     ap.add_argument("--pushpull", action="store_true",
                     help="every worker also receives the updated weights in its own model "
                          "buffer, written by the same fused pass (PushPull)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="ablation: the step as two launches (sum into a merge buffer, then "
+                         "the optimizer); roofline bytes stay the fused method's")
     ap.add_argument("--streaming", action="store_true",
                     help="instead of the throughput line: time the step overlapped with a "
                          "simulated backward pass, one launch vs readiness groups")
@@ -359,6 +367,7 @@ def main(argv=None) -> int:
     import torch
     from paper_1805_07891_amd import workloads
     from paper_1805_07891_amd.job import TorchJob, load_library
+    from paper_1805_07891_amd.phub import PHUB_SCHEDULE_SPLIT
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -381,7 +390,9 @@ def main(argv=None) -> int:
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
         stream = torch.cuda.Stream(device=dev)
-        job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes)
+        job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
+                       chunk_bytes=args.chunk_bytes, unfused=args.unfused,
+                       schedule=None if args.schedule == "lpt" else PHUB_SCHEDULE_SPLIT)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
              for w in range(spec.num_workers)]
@@ -442,7 +453,7 @@ def main(argv=None) -> int:
     med_ms = durs[len(durs) // 2]
     dom_bytes = job_bytes(wl.jobs[dom])
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
-    traffic = None if args.pushpull else measured_traffic(args.workload)
+    traffic = None if (args.pushpull or args.unfused) else measured_traffic(args.workload)
     groups, threads, segs, _ = jobs[dom].info()
     cache_resident = [job.info()[3] for job in jobs]
 
@@ -470,11 +481,13 @@ def main(argv=None) -> int:
             "jobs": [{"name": j.name, "workers": j.num_workers, "keys": j.num_keys,
                       "params": j.num_params, "wm_cache_resident": bool(r)}
                      for j, r in zip(wl.jobs, cache_resident)],
-            "chunk_bytes": wl.jobs[0].chunk_bytes,
+            "chunk_bytes": args.chunk_bytes or wl.jobs[0].chunk_bytes,
+            "schedule": args.schedule,
             "optimizer": {"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
                           "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov},
             "hbm_bytes_per_step": sum(job_bytes(j) for j in wl.jobs),
             "pushpull": args.pushpull,
+            "unfused": args.unfused,
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},
             "host_us_per_step": round(host_s * 1e6 / K, 2),
@@ -482,7 +495,8 @@ def main(argv=None) -> int:
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "fused_step_fixed" if wl.jobs[dom].num_workers <= 16 else "fused_step_any",
+            "kernel": ("aggregate_only + optimize_only" if args.unfused else
+                       "fused_step_fixed" if wl.jobs[dom].num_workers <= 16 else "fused_step_any"),
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

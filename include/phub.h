@@ -118,6 +118,14 @@ typedef struct phub_options {
     const int *key_group;   /* num_keys entries in [0, num_groups), read
                                during phub_init_ex only; ignored when
                                num_groups is 0. */
+    int unfused;            /* ablation of the fused pass (section 3.2.2:
+                               the aggregating thread also optimizes): 1
+                               runs the step as two launches, a sum of the N
+                               gradients into a job-owned merge buffer, then
+                               the optimizer over it ((N + 6) * 4 bytes per
+                               element instead of (N + 4) * 4).  Same
+                               results.  Not with readiness groups or
+                               pushpull (PHUB_EINVAL).  0: fused (default). */
 } phub_options;
 
 /*

@@ -488,6 +488,93 @@ __global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS
     }
 }
 
+// Ablation: the unfused ("wide") form of the step, kept to measure what
+// fusion saves.  Pass 1 sums the N gradients of every element in worker
+// order and writes the sum to a merge buffer laid out like W; pass 2 reads
+// the merge buffer, W and M and runs the optimizer.  Same arithmetic, same
+// schedule, (N + 6) * 4 bytes per element instead of (N + 4) * 4, and two
+// launches.
+__device__ __forceinline__ void aggregate_range(const float* const* kp, int n, int64_t offset,
+                                                float* out, uint32_t nvec, uint32_t rem) {
+    const uint32_t lane = threadIdx.x & 63u;
+    for (uint32_t v = lane; v < nvec; v += 64u) {
+        const uint32_t bo = v * 16u;
+        f4 s = load_stream(kp[0] + offset, bo);
+        for (int w0 = 1; w0 < n; w0 += kBatch) {
+            f4 a[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                if (w0 + j < n) a[j] = load_stream(kp[w0 + j] + offset, bo);
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                if (w0 + j < n) s = s + a[j];
+        }
+        store_out(out, bo, s);
+    }
+    if (lane < rem) {
+        const int64_t i = int64_t(nvec) * 4 + lane;
+        float s = load1(kp[0] + offset, i);
+        for (int w = 1; w < n; ++w) s = s + load1(kp[w] + offset, i);
+        store1(out, i, s);
+    }
+}
+
+template <bool NEST, bool RES>
+__device__ __forceinline__ void optimize_range(const float* sum, float* wb, float* mb,
+                                               uint32_t nvec, uint32_t rem, float nlr, float mu,
+                                               float wd) {
+    const uint32_t lane = threadIdx.x & 63u;
+    for (uint32_t v = lane; v < nvec; v += 64u) {
+        const uint32_t bo = v * 16u;
+        const f4 s = load_stream(sum, bo);
+        f4 wv = load_wm<RES>(wb, bo);
+        f4 mv = load_wm<RES>(mb, bo);
+        optimize4<NEST>(s, wv, mv, nlr, mu, wd);
+        store_wm<RES>(wb, bo, wv);
+        store_wm<RES>(mb, bo, mv);
+    }
+    if (lane < rem) {
+        const int64_t i = int64_t(nvec) * 4 + lane;
+        float wv = load1(wb, i), mv = load1(mb, i);
+        optimize<NEST>(load1(sum, i), wv, mv, nlr, mu, wd);
+        store1(wb, i, wv);
+        store1(mb, i, mv);
+    }
+}
+
+__global__ __launch_bounds__(kBlockThreads) void aggregate_only(PHUB_KERNEL_ARGS, float* merge) {
+    const uint32_t wave = wave_index();
+    const int n = num_workers;
+    for (int32_t t = tile_begin[wave]; t < tile_begin[wave + 1]; ++t) {
+        const DevTile tl = tiles[t];
+        aggregate_range(grads + int64_t(tl.key) * n, n, int64_t(tl.vec) * 4,
+                        merge + tl.arena_offset, uint32_t(kTileElems / 4), 0u);
+    }
+    for (int32_t r = rem_begin[wave]; r < rem_begin[wave + 1]; ++r) {
+        const DevRem rm = rems[r];
+        aggregate_range(grads + int64_t(rm.key) * n, n, rm.offset, merge + rm.arena_offset,
+                        uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u);
+    }
+}
+
+template <bool NEST, bool RES>
+__global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS, float* merge) {
+    const uint32_t wave = wave_index();
+    const float nlr = -lr;
+    for (int32_t t = tile_begin[wave]; t < tile_begin[wave + 1]; ++t) {
+        const DevTile tl = tiles[t];
+        optimize_range<NEST, RES>(merge + tl.arena_offset, weights + tl.arena_offset,
+                                  moments + tl.arena_offset, uint32_t(kTileElems / 4), 0u, nlr,
+                                  mu, wd);
+    }
+    for (int32_t r = rem_begin[wave]; r < rem_begin[wave + 1]; ++r) {
+        const DevRem rm = rems[r];
+        optimize_range<NEST, RES>(merge + rm.arena_offset, weights + rm.arena_offset,
+                                  moments + rm.arena_offset, uint32_t(rm.count) >> 2,
+                                  uint32_t(rm.count) & 3u, nlr, mu, wd);
+    }
+}
+
 #define PHUB_LAUNCH_ARGS                                                                    \
     p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.outs, p.weights, p.moments, p.lr, \
         p.mu, p.wd, p.num_workers
@@ -550,10 +637,27 @@ hipError_t launch_res(const StepParams& p, bool nesterov, int grid, hipStream_t 
     }
 }
 
+template <bool RES>
+hipError_t launch_unfused(const StepParams& p, bool nesterov, int grid, hipStream_t stream) {
+    hipLaunchKernelGGL(aggregate_only, dim3(grid), dim3(kBlockThreads), 0, stream,
+                       PHUB_LAUNCH_ARGS, p.merge);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    if (nesterov)
+        hipLaunchKernelGGL((optimize_only<true, RES>), dim3(grid), dim3(kBlockThreads), 0, stream,
+                           PHUB_LAUNCH_ARGS, p.merge);
+    else
+        hipLaunchKernelGGL((optimize_only<false, RES>), dim3(grid), dim3(kBlockThreads), 0, stream,
+                           PHUB_LAUNCH_ARGS, p.merge);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_fused_step(const StepParams& p, bool nesterov, bool resident, int grid,
                              hipStream_t stream) {
+    if (p.merge)
+        return resident ? launch_unfused<true>(p, nesterov, grid, stream)
+                        : launch_unfused<false>(p, nesterov, grid, stream);
     return resident ? launch_res<true>(p, nesterov, grid, stream)
                     : launch_res<false>(p, nesterov, grid, stream);
 }

@@ -50,6 +50,7 @@ struct StepParams {
     const int32_t* rem_begin;     // wave w owns rems [rem_begin[w], rem_begin[w+1])
     const float* const* grads;    // [row * num_workers + worker], 16-byte aligned
     float* const* outs;           // same layout: model buffers that receive w' (pushpull), or null
+    float* merge;                 // unfused ablation: sum buffer laid out like W, or null (fused)
     float* weights;               // W arena
     float* moments;               // M arena
     float lr;
@@ -60,7 +61,8 @@ struct StepParams {
 
 // Enqueues one fused aggregate + optimize pass over the whole schedule
 // (and, when p.outs is set, writes the updated weights into every worker's
-// model buffer in the same pass):
+// model buffer in the same pass; when p.merge is set, runs the unfused
+// two-pass ablation instead):
 // `grid` workgroups of kBlockThreads threads, one bin per wave (the bin
 // tables have grid * kBlockThreads / 64 + 1 entries).  `resident`: W and M
 // use the cache-allocating policy instead of non-temporal accesses.

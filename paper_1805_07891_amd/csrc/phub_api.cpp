@@ -127,6 +127,7 @@ struct phub_job {
 
     float* weights = nullptr;
     float* moments = nullptr;
+    float* merge = nullptr;  // unfused ablation only: the sum, laid out like W
     phub::DevTile* d_tiles = nullptr;
     int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of bins + 1 entries
     phub::DevRem* d_rems = nullptr;
@@ -184,6 +185,7 @@ void release(phub_job* j) {
     if (j->d_rem_begin) (void)hipFree(j->d_rem_begin);
     if (j->d_rems) (void)hipFree(j->d_rems);
     if (j->moments) (void)hipFree(j->moments);
+    if (j->merge) (void)hipFree(j->merge);
     if (j->weights) (void)hipFree(j->weights);
     for (int i = 0; i < kStageSlots; ++i) {
         if (j->stage_done[i]) (void)hipEventDestroy(j->stage_done[i]);
@@ -277,6 +279,8 @@ int launch_group(phub_job* j, int g) {
     const size_t n = size_t(j->num_workers);
     const int64_t pairs = int64_t(j->rgroup_row_begin[g + 1] - j->rgroup_row_begin[g]) * j->num_workers;
     const bool pull = j->rgroup_outs[g] > 0;
+    if (pull && j->merge)
+        return fail(PHUB_EINVAL, "the unfused variant does not take pushpull");
     if (pull && j->rgroup_outs[g] != pairs) {
         for (size_t i = size_t(j->rgroup_row_begin[g]) * n; i < size_t(j->rgroup_row_begin[g + 1]) * n; ++i)
             if (!j->has_out[i])
@@ -302,13 +306,14 @@ int launch_group(phub_job* j, int g) {
         if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent (ready event)");
     }
     if (j->rgroup_work[g]) {
-        phub::StepParams p;
+        phub::StepParams p{};
         p.tiles = j->d_tiles;
         p.tile_begin = j->d_tile_begin + size_t(g) * (j->bins + 1);
         p.rems = j->d_rems;
         p.rem_begin = j->d_rem_begin + size_t(g) * (j->bins + 1);
         p.grads = j->d_grads;
         p.outs = pull ? j->d_outs : nullptr;
+        p.merge = j->merge;
         p.weights = j->weights;
         p.moments = j->moments;
         p.lr = j->lr;
@@ -434,6 +439,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     int schedule = phub::kScheduleLpt;
     int64_t resident_bytes = -1;  // -1: the shared per-device budget
     int num_rgroups = 0;          // 0: no readiness groups
+    bool unfused = false;
     if (options) {
         if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
@@ -449,9 +455,12 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                     return fail(PHUB_EINVAL, "key_group[%d] = %d is outside [0, %d)", k,
                                 options->key_group[k], options->num_groups);
         }
+        if (options->unfused != 0 && options->num_groups > 0)
+            return fail(PHUB_EINVAL, "the unfused variant does not take readiness groups");
         schedule = options->schedule;
         if (options->resident_bytes >= 0) resident_bytes = options->resident_bytes;
         num_rgroups = options->num_groups;
+        unfused = options->unfused != 0;
     }
 
     phub_job* j = new (std::nothrow) phub_job;
@@ -577,6 +586,12 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             hipMalloc(&j->moments, arena_bytes) != hipSuccess) {
             (void)hipGetLastError();
             rc = fail(PHUB_ENOMEM, "device allocation of W and M (%zu bytes each) failed",
+                      arena_bytes);
+            goto fail_cleanup;
+        }
+        if (unfused && hipMalloc(&j->merge, arena_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            rc = fail(PHUB_ENOMEM, "device allocation of the merge buffer (%zu bytes) failed",
                       arena_bytes);
             goto fail_cleanup;
         }

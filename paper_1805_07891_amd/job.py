@@ -56,7 +56,7 @@ class TorchJob:
     def __init__(self, spec: Job, device, stream=None, chunk_bytes: Optional[int] = None,
                  lib: Optional[_phub.Library] = None, schedule: Optional[int] = None,
                  resident_bytes: Optional[int] = None,
-                 key_group: Optional[Sequence[int]] = None):
+                 key_group: Optional[Sequence[int]] = None, unfused: bool = False):
         import torch
         self.torch = torch
         self.spec = spec
@@ -70,7 +70,7 @@ class TorchJob:
                                              spec.lr, spec.momentum, spec.weight_decay,
                                              spec.nesterov, self.stream.cuda_stream,
                                              schedule=schedule, resident_bytes=resident_bytes,
-                                             key_group=key_group)
+                                             key_group=key_group, unfused=unfused)
         self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers
         self._grad_refs: List = [None] * spec.num_workers

@@ -50,7 +50,8 @@ class PhubSegment(ctypes.Structure):
 
 class PhubOptions(ctypes.Structure):
     _fields_ = [("schedule", ctypes.c_int), ("resident_bytes", ctypes.c_int64),
-                ("num_groups", ctypes.c_int), ("key_group", ctypes.POINTER(ctypes.c_int))]
+                ("num_groups", ctypes.c_int), ("key_group", ctypes.POINTER(ctypes.c_int)),
+                ("unfused", ctypes.c_int)]
 
 
 class Library:
@@ -106,7 +107,8 @@ class Library:
                   lr: float, momentum: float, weight_decay: float, nesterov: bool,
                   hip_stream: Optional[int] = None, check: bool = True,
                   schedule: Optional[int] = None, resident_bytes: Optional[int] = None,
-                  key_group: Optional[Sequence[int]] = None, num_groups: Optional[int] = None):
+                  key_group: Optional[Sequence[int]] = None, num_groups: Optional[int] = None,
+                  unfused: bool = False):
         """Returns the job handle (an int), or (rc, None) with check=False on
         error.  With ``schedule``, ``resident_bytes`` or readiness groups
         (``key_group``: the group of each key; ``num_groups`` defaults to
@@ -116,7 +118,8 @@ class Library:
         args = (ctypes.byref(out), int(num_workers), len(key_elems),
                 ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes), float(lr), float(momentum),
                 float(weight_decay), int(bool(nesterov)), hip_stream)
-        if schedule is None and resident_bytes is None and key_group is None and num_groups is None:
+        if (schedule is None and resident_bytes is None and key_group is None and num_groups is None
+                and not unfused):
             rc = self.lib.phub_init(*args)
         else:
             groups = None
@@ -127,7 +130,8 @@ class Library:
             opts = PhubOptions(PHUB_SCHEDULE_LPT if schedule is None else int(schedule),
                                -1 if resident_bytes is None else int(resident_bytes),
                                0 if num_groups is None else int(num_groups),
-                               ctypes.cast(groups, ctypes.POINTER(ctypes.c_int)) if groups else None)
+                               ctypes.cast(groups, ctypes.POINTER(ctypes.c_int)) if groups else None,
+                               int(bool(unfused)))
             rc = self.lib.phub_init_ex(*args, ctypes.byref(opts))
         if rc != 0:
             self._check(rc, check)

@@ -54,13 +54,14 @@ def _rel_err(x, ref):
 
 def run_small_case(torch, dev, lib, n_workers, key_elems, steps=2, chunk_bytes=32768,
                    lr=0.1, mu=0.9, wd=1e-4, nesterov=True, seed=0, push="keys",
-                   reuse_buffers=False, stream=None, schedule=None, resident_bytes=None):
+                   reuse_buffers=False, stream=None, schedule=None, resident_bytes=None,
+                   unfused=False):
     """Runs `steps` steps on the GPU and in the oracle; returns the job and
     per-step (gpu W, gpu M, oracle W, oracle M) lists per key."""
     spec = Job("case", n_workers, tuple(int(n) for n in key_elems), chunk_elems=chunk_bytes // 4,
                lr=lr, momentum=mu, weight_decay=wd, nesterov=nesterov, sigma_g=1e-2)
     job = TorchJob(spec, dev, stream=stream, chunk_bytes=chunk_bytes, lib=lib, schedule=schedule,
-                   resident_bytes=resident_bytes)
+                   resident_bytes=resident_bytes, unfused=unfused)
     offs, total = key_offsets(spec.key_elems)
     rng = np.random.default_rng(seed)
     w0 = np.zeros(total, np.float32)
@@ -317,6 +318,21 @@ def test_bandwidth_probe_reads_and_leaves_sink(torch_dev):
     torch.cuda.synchronize()
     assert torch.count_nonzero(sink[:64]).item() == 64      # wave 0 read the single tile
     assert torch.count_nonzero(sink[64:]).item() == 0
+
+
+@pytest.mark.parametrize("n", [1, 4, 8, 16, 17])
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_unfused_variant_gives_the_same_bits(lib, torch_dev, n, nesterov):
+    """The two-pass ablation (sum into a merge buffer, then the optimizer)
+    performs the same operations in the same order."""
+    torch, dev = torch_dev
+    keys = (5, 1024, 8193, 40000, 3, 70001, 1)
+    _say("unfused N", n, "nesterov", nesterov)
+    for resident in (0, 1 << 40):
+        job, res = run_small_case(torch, dev, lib, n, keys, steps=2, nesterov=nesterov,
+                                  seed=40 + n, resident_bytes=resident, unfused=True)
+        assert_parity(res, f"unfused N={n} nesterov={nesterov} resident={resident}")
+        job.destroy()
 
 
 def test_set_weights_resets_momentum(lib, torch_dev):

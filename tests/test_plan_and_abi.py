@@ -242,15 +242,17 @@ def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
     for kw in [dict(num_workers=0), dict(chunk_bytes=20), dict(lr=float("nan")),
                dict(momentum=float("inf")), dict(schedule=7), dict(resident_bytes=-2),
                dict(key_group=[0, 2], num_groups=2), dict(key_group=[0, -1]),
-               dict(key_group=[0, 1], num_groups=-1), dict(key_group=None, num_groups=3)]:
+               dict(key_group=[0, 1], num_groups=-1), dict(key_group=None, num_groups=3),
+               dict(key_group=[0, 1], unfused=True)]:
         a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
                  weight_decay=1e-4, nesterov=True, schedule=None, resident_bytes=None,
-                 key_group=None, num_groups=None)
+                 key_group=None, num_groups=None, unfused=False)
         a.update(kw)
         rc, h = lib.phub_init(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["lr"],
                               a["momentum"], a["weight_decay"], a["nesterov"], check=False,
                               schedule=a["schedule"], resident_bytes=a["resident_bytes"],
-                              key_group=a["key_group"], num_groups=a["num_groups"])
+                              key_group=a["key_group"], num_groups=a["num_groups"],
+                              unfused=a["unfused"])
         assert rc == phub.PHUB_EINVAL and h is None, kw
 
 
