@@ -43,6 +43,12 @@ class OracleLib:
         lib.oracle_step_f64.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp, vp, vp,
                                         ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int]
         lib.oracle_step_f64.restype = ctypes.c_int
+        f32 = ctypes.c_float
+        lib.oracle_step_sgd_f32.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp, vp, f32, f32]
+        lib.oracle_step_sgd_f32.restype = ctypes.c_int
+        lib.oracle_step_adam_f32.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp,
+                                             f32, f32, f32, f32, f32, ctypes.c_int64]
+        lib.oracle_step_adam_f32.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -85,6 +91,47 @@ class OracleLib:
         if rc != 0:
             raise ValueError(f"oracle rejected its arguments (code {rc})")
 
+    def _check_args(self, grads, weights, states):
+        num_workers, num_keys = len(grads), len(weights)
+        if num_workers < 1 or num_keys < 1:
+            raise ValueError("need at least one worker and one key")
+        elems = np.array([a.size for a in weights], dtype=np.int64)
+        flat_g = []
+        for w in range(num_workers):
+            if len(grads[w]) != num_keys:
+                raise ValueError("every worker must give one gradient per key")
+            flat_g.extend(grads[w][k] for k in range(num_keys))
+        for st in states:
+            if len(st) != num_keys or any(st[k].size != elems[k] for k in range(num_keys)):
+                raise ValueError("one state array per key, of the key's length")
+        for a in flat_g + list(weights) + [x for st in states for x in st]:
+            if a.dtype != np.float32 or not a.flags.c_contiguous or a.ndim != 1:
+                raise ValueError("oracle arrays must be contiguous 1-D float32")
+        for k in range(num_keys):
+            if any(grads[w][k].size != elems[k] for w in range(num_workers)):
+                raise ValueError(f"key {k}: length mismatch")
+        return num_workers, num_keys, elems, flat_g
+
+    def step_sgd(self, grads, weights, lr, weight_decay):
+        """One step with plain SGD (no state), in place on ``weights`` (fp32)."""
+        n, k, elems, flat_g = self._check_args(grads, weights, [])
+        rc = self.lib.oracle_step_sgd_f32(n, k, elems.ctypes.data, _ptrs(flat_g), _ptrs(weights),
+                                          float(np.float32(lr)), float(np.float32(weight_decay)))
+        if rc != 0:
+            raise ValueError(f"oracle rejected its arguments (code {rc})")
+
+    def step_adam(self, grads, weights, m1, m2, lr, beta1, beta2, eps, weight_decay, step):
+        """Step number ``step`` (from 1) of Adam, in place on ``weights`` and
+        the two moment arrays ``m1``, ``m2`` (fp32)."""
+        n, k, elems, flat_g = self._check_args(grads, weights, [m1, m2])
+        rc = self.lib.oracle_step_adam_f32(n, k, elems.ctypes.data, _ptrs(flat_g), _ptrs(weights),
+                                           _ptrs(m1), _ptrs(m2), float(np.float32(lr)),
+                                           float(np.float32(beta1)), float(np.float32(beta2)),
+                                           float(np.float32(eps)), float(np.float32(weight_decay)),
+                                           int(step))
+        if rc != 0:
+            raise ValueError(f"oracle rejected its arguments (code {rc})")
+
     def step_flat(self, grads, weight, mom, lr, momentum, weight_decay, nesterov, dtype=np.float32):
         """One step over a single flat array (one key): grads[w] is worker w's."""
         self.step([[g] for g in grads], [weight], [mom], lr, momentum, weight_decay, nesterov, dtype)
@@ -120,3 +167,13 @@ def step_flat(grads: Sequence[np.ndarray], weight: np.ndarray, mom: np.ndarray, 
               momentum: float, weight_decay: float, nesterov: bool, dtype=np.float32) -> None:
     """One step over a single flat array (one key): grads[w] is worker w's."""
     _load().step_flat(grads, weight, mom, lr, momentum, weight_decay, nesterov, dtype)
+
+
+def step_sgd(grads, weights, lr, weight_decay) -> None:
+    """Plain SGD step of the fp32 oracle; see ``OracleLib.step_sgd``."""
+    _load().step_sgd(grads, weights, lr, weight_decay)
+
+
+def step_adam(grads, weights, m1, m2, lr, beta1, beta2, eps, weight_decay, step) -> None:
+    """Adam step of the fp32 oracle; see ``OracleLib.step_adam``."""
+    _load().step_adam(grads, weights, m1, m2, lr, beta1, beta2, eps, weight_decay, step)
