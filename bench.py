@@ -337,6 +337,8 @@ def main(argv=None) -> int:
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
+    ap.add_argument("--optimizer", choices=("momentum", "sgd", "adam"), default="momentum",
+                    help="the pluggable optimizer (default: the workload's Nesterov momentum)")
     ap.add_argument("--pushpull", action="store_true",
                     help="every worker also receives the updated weights in its own model "
                          "buffer, written by the same fused pass (PushPull)")
@@ -392,6 +394,7 @@ def main(argv=None) -> int:
         stream = torch.cuda.Stream(device=dev)
         job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
                        chunk_bytes=args.chunk_bytes, unfused=args.unfused,
+                       optimizer=None if args.optimizer == "momentum" else args.optimizer,
                        schedule=None if args.schedule == "lpt" else PHUB_SCHEDULE_SPLIT)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
@@ -437,9 +440,13 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
+    states = {"momentum": 2, "sgd": 1, "adam": 3}[args.optimizer]
+
     def job_bytes(spec):
-        # the fused pass writes w' once more per worker with pushpull
-        return spec.hbm_bytes_per_step() + (spec.worker_grad_bytes_per_step() if args.pushpull else 0)
+        # N gradient reads, each state array read and written, and with
+        # pushpull w' written once more per worker
+        return (spec.num_workers + 2 * states) * spec.num_params * 4 + \
+            (spec.worker_grad_bytes_per_step() if args.pushpull else 0)
 
     ms_per_step = (t1 - t0) * 1e3 / K
     worker_bytes = wl.worker_grad_bytes_per_step()
@@ -453,7 +460,8 @@ def main(argv=None) -> int:
     med_ms = durs[len(durs) // 2]
     dom_bytes = job_bytes(wl.jobs[dom])
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
-    traffic = None if (args.pushpull or args.unfused) else measured_traffic(args.workload)
+    traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum")
+               else measured_traffic(args.workload))
     groups, threads, segs, _ = jobs[dom].info()
     cache_resident = [job.info()[3] for job in jobs]
 
@@ -483,10 +491,15 @@ def main(argv=None) -> int:
                      for j, r in zip(wl.jobs, cache_resident)],
             "chunk_bytes": args.chunk_bytes or wl.jobs[0].chunk_bytes,
             "schedule": args.schedule,
-            "optimizer": {"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
-                          "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov},
+            "optimizer": ({"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
+                           "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov}
+                          if args.optimizer == "momentum" else
+                          {"kind": args.optimizer, "lr": wl.jobs[0].lr,
+                           "weight_decay": wl.jobs[0].weight_decay,
+                           **({"betas": [0.9, 0.999], "eps": 1e-8} if args.optimizer == "adam" else {})}),
             "hbm_bytes_per_step": sum(job_bytes(j) for j in wl.jobs),
             "pushpull": args.pushpull,
+            "optimizer_kind": args.optimizer,
             "unfused": args.unfused,
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},

@@ -88,6 +88,18 @@ enum phub_schedule {
     PHUB_SCHEDULE_LPT = 1    /* the paper's balanced partition of chunks (default) */
 };
 
+/* Optimizers (section 3.2.2: aggregators and optimizers are pluggable).
+ * All take the same aggregated gradient s and coupled L2 weight decay wd:
+ * d = s + wd*w. */
+enum phub_optimizer {
+    PHUB_OPT_MOMENTUM = 0, /* SGD with momentum: phub_init's momentum and
+                              nesterov arguments (section 4.2; default) */
+    PHUB_OPT_SGD = 1,      /* plain SGD, no state: w' = w - lr*d */
+    PHUB_OPT_ADAM = 2      /* Adam with bias correction (beta1, beta2, eps
+                              below; state M and V); the step number t counts
+                              the job's completed phub_step calls, from 1 */
+};
+
 /* Optional settings of phub_init_ex. */
 typedef struct phub_options {
     int schedule;           /* a phub_schedule value */
@@ -118,6 +130,12 @@ typedef struct phub_options {
     const int *key_group;   /* num_keys entries in [0, num_groups), read
                                during phub_init_ex only; ignored when
                                num_groups is 0. */
+    int optimizer;          /* a phub_optimizer value (0: momentum SGD) */
+    float beta1, beta2;     /* Adam: moment decay rates, each in [0, 1) */
+    float eps;              /* Adam: added to the root of the second moment
+                               (finite, >= 0).  The three are ignored by the
+                               other optimizers; momentum and nesterov of
+                               phub_init_ex are ignored by SGD and Adam. */
     int unfused;            /* ablation of the fused pass (section 3.2.2:
                                the aggregating thread also optimizes): 1
                                runs the step as two launches, a sum of the N
@@ -251,10 +269,18 @@ int phub_pull(phub_job *job, int key, const float **weights);
 
 /*
  * phub_get_state - device pointers to key `key`'s master weights and
- * momentum (n_k fp32 each, job-owned, same validity as phub_pull).  Either
- * output may be NULL.  Errors: PHUB_EINVAL, PHUB_ESTATE.
+ * momentum (Adam: first moment; plain SGD: NULL), n_k fp32 each,
+ * job-owned, same validity as phub_pull.  Either output may be NULL.
+ * Errors: PHUB_EINVAL, PHUB_ESTATE.
  */
 int phub_get_state(phub_job *job, int key, const float **weights, const float **momentum);
+
+/*
+ * phub_get_second_moment - device pointer to key `key`'s second moment
+ * (Adam), or NULL for the other optimizers.  Errors: PHUB_EINVAL,
+ * PHUB_ESTATE.
+ */
+int phub_get_second_moment(phub_job *job, int key, const float **second);
 
 /*
  * phub_sync - wait on the host until all work enqueued by the job has run.

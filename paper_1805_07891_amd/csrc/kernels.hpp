@@ -43,6 +43,24 @@ struct DevRem {
 };
 static_assert(sizeof(DevRem) == 32, "DevRem layout");
 
+// Optimizers of the fused pass (pluggable, paper section 3.2.2).
+enum OptKind : int {
+    kOptMomentum = 0,  // SGD with momentum (state W, M)
+    kOptNesterov = 1,  // SGD with Nesterov momentum (state W, M)
+    kOptSgd = 2,       // plain SGD (state W)
+    kOptAdam = 3,      // Adam with bias correction (state W, M, V)
+};
+
+// Scalars of one launch.  For Adam, c1 = 1 - b1, c2 = 1 - b2 and the
+// step's bias corrections k1 = lr / (1 - b1^t), k2 = 1 / (1 - b2^t) are
+// computed on the host in double and rounded to fp32 once.
+struct OptArgs {
+    float nlr;  // -lr
+    float mu;
+    float wd;
+    float b1, b2, c1, c2, k1, k2, eps;
+};
+
 struct StepParams {
     const DevTile* tiles;         // grouped by bin (one bin per wave)
     const int32_t* tile_begin;    // wave w owns tiles [tile_begin[w], tile_begin[w+1])
@@ -52,21 +70,20 @@ struct StepParams {
     float* const* outs;           // same layout: model buffers that receive w' (pushpull), or null
     float* merge;                 // unfused ablation: sum buffer laid out like W, or null (fused)
     float* weights;               // W arena
-    float* moments;               // M arena
-    float lr;
-    float mu;
-    float wd;
+    float* moments;               // M arena (momentum, Adam's first moment), or null
+    float* second;                // V arena (Adam's second moment), or null
+    OptArgs opt;
     int num_workers;
 };
 
 // Enqueues one fused aggregate + optimize pass over the whole schedule
 // (and, when p.outs is set, writes the updated weights into every worker's
 // model buffer in the same pass; when p.merge is set, runs the unfused
-// two-pass ablation instead):
-// `grid` workgroups of kBlockThreads threads, one bin per wave (the bin
-// tables have grid * kBlockThreads / 64 + 1 entries).  `resident`: W and M
-// use the cache-allocating policy instead of non-temporal accesses.
-hipError_t launch_fused_step(const StepParams& p, bool nesterov, bool resident, int grid,
+// two-pass ablation instead): `grid` workgroups of kBlockThreads threads,
+// one bin per wave (the bin tables have grid * kBlockThreads / 64 + 1
+// entries).  `optimizer` is an OptKind.  `resident`: the state uses the
+// cache-allocating policy instead of non-temporal accesses.
+hipError_t launch_fused_step(const StepParams& p, int optimizer, bool resident, int grid,
                              hipStream_t stream);
 
 }  // namespace phub

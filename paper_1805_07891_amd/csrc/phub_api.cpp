@@ -96,6 +96,9 @@ struct phub_job {
     int64_t chunk_bytes = 0;
     float lr = 0, mu = 0, wd = 0;
     bool nesterov = false;
+    int opt = phub::kOptNesterov;  // an OptKind
+    float b1 = 0, b2 = 0, eps = 0;  // Adam
+    int64_t steps_done = 0;         // completed steps (Adam's bias correction)
 
     int device = 0;
     hipStream_t stream = nullptr;
@@ -126,7 +129,8 @@ struct phub_job {
     std::vector<uint8_t> rgroup_out_dirty;
 
     float* weights = nullptr;
-    float* moments = nullptr;
+    float* moments = nullptr;  // null for plain SGD
+    float* second = nullptr;   // Adam's second moment, else null
     float* merge = nullptr;  // unfused ablation only: the sum, laid out like W
     phub::DevTile* d_tiles = nullptr;
     int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of bins + 1 entries
@@ -185,6 +189,7 @@ void release(phub_job* j) {
     if (j->d_rem_begin) (void)hipFree(j->d_rem_begin);
     if (j->d_rems) (void)hipFree(j->d_rems);
     if (j->moments) (void)hipFree(j->moments);
+    if (j->second) (void)hipFree(j->second);
     if (j->merge) (void)hipFree(j->merge);
     if (j->weights) (void)hipFree(j->weights);
     for (int i = 0; i < kStageSlots; ++i) {
@@ -272,6 +277,27 @@ int upload_out_rows(phub_job* j, int g) {
     return PHUB_OK;
 }
 
+// Scalars of this step's launches.  Adam's are derived from the fp32
+// hyperparameters in double and rounded to fp32 once; the step number
+// counts from 1 for each job.
+phub::OptArgs optimizer_args(const phub_job* j) {
+    phub::OptArgs o{};
+    o.nlr = -j->lr;
+    o.mu = j->mu;
+    o.wd = j->wd;
+    if (j->opt == phub::kOptAdam) {
+        const double t = double(j->steps_done + 1);
+        o.b1 = j->b1;
+        o.b2 = j->b2;
+        o.c1 = float(1.0 - double(j->b1));
+        o.c2 = float(1.0 - double(j->b2));
+        o.k1 = float(double(j->lr) / (1.0 - std::pow(double(j->b1), t)));
+        o.k2 = float(1.0 / (1.0 - std::pow(double(j->b2), t)));
+        o.eps = j->eps;
+    }
+    return o;
+}
+
 // Enqueues group g: its pointer rows if they changed, a wait for every
 // distinct ready event of its pushes, then the fused kernel over its
 // schedule.
@@ -316,11 +342,10 @@ int launch_group(phub_job* j, int g) {
         p.merge = j->merge;
         p.weights = j->weights;
         p.moments = j->moments;
-        p.lr = j->lr;
-        p.mu = j->mu;
-        p.wd = j->wd;
+        p.second = j->second;
+        p.opt = optimizer_args(j);
         p.num_workers = j->num_workers;
-        hipError_t e = phub::launch_fused_step(p, j->nesterov, j->resident, j->groups, j->stream);
+        hipError_t e = phub::launch_fused_step(p, j->opt, j->resident, j->groups, j->stream);
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
     }
     j->rgroup_launched[g] = 1;
@@ -440,6 +465,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     int64_t resident_bytes = -1;  // -1: the shared per-device budget
     int num_rgroups = 0;          // 0: no readiness groups
     bool unfused = false;
+    int optimizer = PHUB_OPT_MOMENTUM;
+    float beta1 = 0, beta2 = 0, eps = 0;
     if (options) {
         if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
@@ -457,6 +484,20 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         }
         if (options->unfused != 0 && options->num_groups > 0)
             return fail(PHUB_EINVAL, "the unfused variant does not take readiness groups");
+        if (options->optimizer != PHUB_OPT_MOMENTUM && options->optimizer != PHUB_OPT_SGD &&
+            options->optimizer != PHUB_OPT_ADAM)
+            return fail(PHUB_EINVAL, "unknown optimizer %d", options->optimizer);
+        if (options->optimizer == PHUB_OPT_ADAM) {
+            if (!(options->beta1 >= 0.0f && options->beta1 < 1.0f) ||
+                !(options->beta2 >= 0.0f && options->beta2 < 1.0f))
+                return fail(PHUB_EINVAL, "Adam needs 0 <= beta1, beta2 < 1");
+            if (!(options->eps >= 0.0f) || !std::isfinite(options->eps))
+                return fail(PHUB_EINVAL, "Adam needs a finite eps >= 0");
+        }
+        optimizer = options->optimizer;
+        beta1 = options->beta1;
+        beta2 = options->beta2;
+        eps = options->eps;
         schedule = options->schedule;
         if (options->resident_bytes >= 0) resident_bytes = options->resident_bytes;
         num_rgroups = options->num_groups;
@@ -480,6 +521,13 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->mu = momentum;
         j->wd = weight_decay;
         j->nesterov = nesterov != 0;
+        j->opt = optimizer == PHUB_OPT_SGD    ? phub::kOptSgd
+                 : optimizer == PHUB_OPT_ADAM ? phub::kOptAdam
+                 : j->nesterov                ? phub::kOptNesterov
+                                              : phub::kOptMomentum;
+        j->b1 = beta1;
+        j->b2 = beta2;
+        j->eps = eps;
         j->grads.assign(size_t(num_workers) * num_keys, nullptr);
         j->ready.assign(size_t(num_workers) * num_keys, nullptr);
         j->pushed.assign(size_t(num_workers) * num_keys, 0);
@@ -562,7 +610,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->bins = bins;
     }
     j->schedule = schedule;
-    const int64_t wm_bytes = 2 * j->arena_elems * int64_t(sizeof(float));
+    const int num_states = j->opt == phub::kOptSgd ? 1 : j->opt == phub::kOptAdam ? 3 : 2;
+    const int64_t wm_bytes = num_states * j->arena_elems * int64_t(sizeof(float));
     if (resident_bytes >= 0) j->resident = wm_bytes > 0 && wm_bytes <= resident_bytes;
 
 #define PHUB_TRY(call, what)                 \
@@ -583,9 +632,10 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         }
         const size_t arena_bytes = size_t(std::max<int64_t>(j->arena_elems, 1)) * sizeof(float);
         if (hipMalloc(&j->weights, arena_bytes) != hipSuccess ||
-            hipMalloc(&j->moments, arena_bytes) != hipSuccess) {
+            (num_states >= 2 && hipMalloc(&j->moments, arena_bytes) != hipSuccess) ||
+            (num_states >= 3 && hipMalloc(&j->second, arena_bytes) != hipSuccess)) {
             (void)hipGetLastError();
-            rc = fail(PHUB_ENOMEM, "device allocation of W and M (%zu bytes each) failed",
+            rc = fail(PHUB_ENOMEM, "device allocation of the optimizer state (%zu bytes per array) failed",
                       arena_bytes);
             goto fail_cleanup;
         }
@@ -596,7 +646,10 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             goto fail_cleanup;
         }
         PHUB_TRY(hipMemsetAsync(j->weights, 0, arena_bytes, j->stream), "hipMemsetAsync(W)");
-        PHUB_TRY(hipMemsetAsync(j->moments, 0, arena_bytes, j->stream), "hipMemsetAsync(M)");
+        if (j->moments)
+            PHUB_TRY(hipMemsetAsync(j->moments, 0, arena_bytes, j->stream), "hipMemsetAsync(M)");
+        if (j->second)
+            PHUB_TRY(hipMemsetAsync(j->second, 0, arena_bytes, j->stream), "hipMemsetAsync(V)");
 
         // Device form of the schedules: each bin's segments become full tiles
         // (the kernel's straight-line hot loop) and at most one remainder
@@ -710,8 +763,11 @@ int phub_set_weights(phub_job* j, int key, const float* src) {
     hipError_t e = hipMemcpyAsync(j->weights + j->arena_offset[key], src, bytes, hipMemcpyDefault,
                                   j->stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(set_weights)");
-    e = hipMemsetAsync(j->moments + j->arena_offset[key], 0, bytes, j->stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(momentum)");
+    for (float* st : {j->moments, j->second}) {
+        if (!st) continue;
+        e = hipMemsetAsync(st + j->arena_offset[key], 0, bytes, j->stream);
+        if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(optimizer state)");
+    }
     return PHUB_OK;
 }
 
@@ -796,6 +852,7 @@ int phub_step(phub_job* j) {
     std::fill(j->has_out.begin(), j->has_out.end(), 0);
     std::fill(j->rgroup_outs.begin(), j->rgroup_outs.end(), 0);
     j->num_pushed = 0;
+    ++j->steps_done;
     if (j->stage_claimed) {
         j->stage_slot = (j->stage_slot + 1) % kStageSlots;
         j->stage_claimed = false;
@@ -815,7 +872,15 @@ int phub_get_state(phub_job* j, int key, const float** weights, const float** mo
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     if (int rc = check_key(j, key)) return rc;
     if (weights) *weights = j->weights + j->arena_offset[key];
-    if (momentum) *momentum = j->moments + j->arena_offset[key];
+    if (momentum) *momentum = j->moments ? j->moments + j->arena_offset[key] : nullptr;
+    return PHUB_OK;
+}
+
+int phub_get_second_moment(phub_job* j, int key, const float** second) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (int rc = check_key(j, key)) return rc;
+    if (!second) return fail(PHUB_EINVAL, "second is NULL");
+    *second = j->second ? j->second + j->arena_offset[key] : nullptr;
     return PHUB_OK;
 }
 

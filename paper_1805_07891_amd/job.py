@@ -56,7 +56,8 @@ class TorchJob:
     def __init__(self, spec: Job, device, stream=None, chunk_bytes: Optional[int] = None,
                  lib: Optional[_phub.Library] = None, schedule: Optional[int] = None,
                  resident_bytes: Optional[int] = None,
-                 key_group: Optional[Sequence[int]] = None, unfused: bool = False):
+                 key_group: Optional[Sequence[int]] = None, unfused: bool = False,
+                 optimizer: Optional[str] = None, betas=(0.9, 0.999), eps: float = 1e-8):
         import torch
         self.torch = torch
         self.spec = spec
@@ -70,7 +71,11 @@ class TorchJob:
                                              spec.lr, spec.momentum, spec.weight_decay,
                                              spec.nesterov, self.stream.cuda_stream,
                                              schedule=schedule, resident_bytes=resident_bytes,
-                                             key_group=key_group, unfused=unfused)
+                                             key_group=key_group, unfused=unfused,
+                                             optimizer=None if optimizer is None
+                                             else _phub.OPTIMIZERS[optimizer],
+                                             beta1=betas[0], beta2=betas[1], eps=eps)
+        self.optimizer = optimizer or "momentum"
         self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers
         self._grad_refs: List = [None] * spec.num_workers
@@ -158,14 +163,27 @@ class TorchJob:
 
     # -- outputs ---------------------------------------------------------------
     def state_arenas(self):
-        """(W, M) copied to host as numpy arenas of arena_elems values."""
+        """(W, M) copied to host as numpy arenas of arena_elems values (M is
+        None for plain SGD; for Adam it is the first moment)."""
         self.sync()
         w_ptr, m_ptr = self.lib.phub_get_state(self.handle, 0)
         W = np.empty(self.arena_elems, dtype=np.float32)
-        M = np.empty(self.arena_elems, dtype=np.float32)
         copy_to_host(W, w_ptr)
-        copy_to_host(M, m_ptr)
+        M = None
+        if m_ptr:
+            M = np.empty(self.arena_elems, dtype=np.float32)
+            copy_to_host(M, m_ptr)
         return W, M
+
+    def second_moment_arena(self):
+        """Adam's second moment V as a host arena (None for other optimizers)."""
+        self.sync()
+        v_ptr = self.lib.phub_get_second_moment(self.handle, 0)
+        if not v_ptr:
+            return None
+        V = np.empty(self.arena_elems, dtype=np.float32)
+        copy_to_host(V, v_ptr)
+        return V
 
     def split(self, arena: np.ndarray) -> List[np.ndarray]:
         return [arena[o:o + n] for o, n in zip(self.offsets, self.spec.key_elems)]

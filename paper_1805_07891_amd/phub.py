@@ -30,10 +30,16 @@ STATUS_NAMES = {0: "PHUB_OK", -1: "PHUB_EINVAL", -2: "PHUB_ENOTREADY", -3: "PHUB
 PHUB_SCHEDULE_SPLIT = 0
 PHUB_SCHEDULE_LPT = 1
 
+PHUB_OPT_MOMENTUM = 0
+PHUB_OPT_SGD = 1
+PHUB_OPT_ADAM = 2
+OPTIMIZERS = {"momentum": PHUB_OPT_MOMENTUM, "sgd": PHUB_OPT_SGD, "adam": PHUB_OPT_ADAM}
+
 # Every symbol the header declares.
 EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_push_event",
             "phub_push_keys", "phub_push_keys_event", "phub_pushpull", "phub_pushpull_keys",
-            "phub_step", "phub_pull", "phub_get_state", "phub_sync", "phub_get_stream",
+            "phub_step", "phub_pull", "phub_get_state", "phub_get_second_moment", "phub_sync",
+            "phub_get_stream",
             "phub_job_info", "phub_destroy", "phub_last_error", "phub_plan_count",
             "phub_plan_build")
 
@@ -51,7 +57,8 @@ class PhubSegment(ctypes.Structure):
 class PhubOptions(ctypes.Structure):
     _fields_ = [("schedule", ctypes.c_int), ("resident_bytes", ctypes.c_int64),
                 ("num_groups", ctypes.c_int), ("key_group", ctypes.POINTER(ctypes.c_int)),
-                ("unfused", ctypes.c_int)]
+                ("optimizer", ctypes.c_int), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("unfused", ctypes.c_int)]
 
 
 class Library:
@@ -78,6 +85,7 @@ class Library:
             "phub_step": ([vp], i32),
             "phub_pull": ([vp, i32, pp], i32),
             "phub_get_state": ([vp, i32, pp, pp], i32),
+            "phub_get_second_moment": ([vp, i32, pp], i32),
             "phub_sync": ([vp], i32),
             "phub_get_stream": ([vp, pp], i32),
             "phub_job_info": ([vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64),
@@ -108,7 +116,8 @@ class Library:
                   hip_stream: Optional[int] = None, check: bool = True,
                   schedule: Optional[int] = None, resident_bytes: Optional[int] = None,
                   key_group: Optional[Sequence[int]] = None, num_groups: Optional[int] = None,
-                  unfused: bool = False):
+                  unfused: bool = False, optimizer: Optional[int] = None, beta1: float = 0.9,
+                  beta2: float = 0.999, eps: float = 1e-8):
         """Returns the job handle (an int), or (rc, None) with check=False on
         error.  With ``schedule``, ``resident_bytes`` or readiness groups
         (``key_group``: the group of each key; ``num_groups`` defaults to
@@ -119,7 +128,7 @@ class Library:
                 ctypes.cast(elems, ctypes.c_void_p), int(chunk_bytes), float(lr), float(momentum),
                 float(weight_decay), int(bool(nesterov)), hip_stream)
         if (schedule is None and resident_bytes is None and key_group is None and num_groups is None
-                and not unfused):
+                and not unfused and optimizer is None):
             rc = self.lib.phub_init(*args)
         else:
             groups = None
@@ -131,7 +140,8 @@ class Library:
                                -1 if resident_bytes is None else int(resident_bytes),
                                0 if num_groups is None else int(num_groups),
                                ctypes.cast(groups, ctypes.POINTER(ctypes.c_int)) if groups else None,
-                               int(bool(unfused)))
+                               PHUB_OPT_MOMENTUM if optimizer is None else int(optimizer),
+                               float(beta1), float(beta2), float(eps), int(bool(unfused)))
             rc = self.lib.phub_init_ex(*args, ctypes.byref(opts))
         if rc != 0:
             self._check(rc, check)
@@ -203,6 +213,11 @@ class Library:
         w, m = ctypes.c_void_p(), ctypes.c_void_p()
         self._check(self.lib.phub_get_state(job, int(key), ctypes.byref(w), ctypes.byref(m)), True)
         return (w.value or 0), (m.value or 0)
+
+    def phub_get_second_moment(self, job, key: int) -> int:
+        v = ctypes.c_void_p()
+        self._check(self.lib.phub_get_second_moment(job, int(key), ctypes.byref(v)), True)
+        return v.value or 0
 
     def phub_sync(self, job, check: bool = True) -> int:
         return self._check(self.lib.phub_sync(job), check)
