@@ -136,6 +136,11 @@ typedef struct phub_options {
                                (finite, >= 0).  The three are ignored by the
                                other optimizers; momentum and nesterov of
                                phub_init_ex are ignored by SGD and Adam. */
+    int workgroups;         /* persistent workgroups of the job's launch (each
+                               a wave per SIMD of one compute unit); 0: one
+                               per compute unit.  Fewer let concurrent
+                               tenants share the chip without each keeping a
+                               full grid of loads in flight. */
     int unfused;            /* ablation of the fused pass (section 3.2.2:
                                the aggregating thread also optimizes): 1
                                runs the step as two launches, a sum of the N

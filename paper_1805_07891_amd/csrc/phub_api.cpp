@@ -467,7 +467,11 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     bool unfused = false;
     int optimizer = PHUB_OPT_MOMENTUM;
     float beta1 = 0, beta2 = 0, eps = 0;
+    int workgroups = 0;  // 0: one per compute unit
     if (options) {
+        if (options->workgroups < 0)
+            return fail(PHUB_EINVAL, "workgroups must be >= 0, got %d", options->workgroups);
+        workgroups = options->workgroups;
         if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
         if (options->resident_bytes < -1)
@@ -576,7 +580,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     // One schedule per readiness group, over the group's keys in row order.
     std::vector<phub::Plan> plans;
     {
-        const int groups = cus * PHUB_GROUPS_PER_CU;
+        const int groups = workgroups > 0 ? workgroups : cus * PHUB_GROUPS_PER_CU;
         const int bins = groups * (phub::kBlockThreads / 64);
         std::string err;
         try {

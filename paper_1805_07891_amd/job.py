@@ -57,7 +57,8 @@ class TorchJob:
                  lib: Optional[_phub.Library] = None, schedule: Optional[int] = None,
                  resident_bytes: Optional[int] = None,
                  key_group: Optional[Sequence[int]] = None, unfused: bool = False,
-                 optimizer: Optional[str] = None, betas=(0.9, 0.999), eps: float = 1e-8):
+                 optimizer: Optional[str] = None, betas=(0.9, 0.999), eps: float = 1e-8,
+                 workgroups: Optional[int] = None):
         import torch
         self.torch = torch
         self.spec = spec
@@ -74,7 +75,8 @@ class TorchJob:
                                              key_group=key_group, unfused=unfused,
                                              optimizer=None if optimizer is None
                                              else _phub.OPTIMIZERS[optimizer],
-                                             beta1=betas[0], beta2=betas[1], eps=eps)
+                                             beta1=betas[0], beta2=betas[1], eps=eps,
+                                             workgroups=workgroups)
         self.optimizer = optimizer or "momentum"
         self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers

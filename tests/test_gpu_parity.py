@@ -55,13 +55,13 @@ def _rel_err(x, ref):
 def run_small_case(torch, dev, lib, n_workers, key_elems, steps=2, chunk_bytes=32768,
                    lr=0.1, mu=0.9, wd=1e-4, nesterov=True, seed=0, push="keys",
                    reuse_buffers=False, stream=None, schedule=None, resident_bytes=None,
-                   unfused=False):
+                   unfused=False, workgroups=None):
     """Runs `steps` steps on the GPU and in the oracle; returns the job and
     per-step (gpu W, gpu M, oracle W, oracle M) lists per key."""
     spec = Job("case", n_workers, tuple(int(n) for n in key_elems), chunk_elems=chunk_bytes // 4,
                lr=lr, momentum=mu, weight_decay=wd, nesterov=nesterov, sigma_g=1e-2)
     job = TorchJob(spec, dev, stream=stream, chunk_bytes=chunk_bytes, lib=lib, schedule=schedule,
-                   resident_bytes=resident_bytes, unfused=unfused)
+                   resident_bytes=resident_bytes, unfused=unfused, workgroups=workgroups)
     offs, total = key_offsets(spec.key_elems)
     rng = np.random.default_rng(seed)
     w0 = np.zeros(total, np.float32)
@@ -332,6 +332,21 @@ def test_unfused_variant_gives_the_same_bits(lib, torch_dev, n, nesterov):
         job, res = run_small_case(torch, dev, lib, n, keys, steps=2, nesterov=nesterov,
                                   seed=40 + n, resident_bytes=resident, unfused=True)
         assert_parity(res, f"unfused N={n} nesterov={nesterov} resident={resident}")
+        job.destroy()
+
+
+@pytest.mark.parametrize("workgroups", [1, 7, 64, 1000])
+def test_launch_size_does_not_change_results(lib, torch_dev, workgroups):
+    """Any persistent grid (fewer or more workgroups than compute units)
+    covers the whole schedule once."""
+    torch, dev = torch_dev
+    keys = (5, 1024, 8193, 40000, 3, 70001, 1 << 20)
+    _say("workgroups", workgroups)
+    for resident in (0, 1 << 40):
+        job, res = run_small_case(torch, dev, lib, 8, keys, steps=2, seed=70 + workgroups,
+                                  resident_bytes=resident, workgroups=workgroups)
+        assert job.info()[0] == workgroups
+        assert_parity(res, f"workgroups={workgroups} resident={resident}")
         job.destroy()
 
 

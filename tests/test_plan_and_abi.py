@@ -245,18 +245,19 @@ def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
                dict(key_group=[0, 1], num_groups=-1), dict(key_group=None, num_groups=3),
                dict(key_group=[0, 1], unfused=True), dict(optimizer=7),
                dict(optimizer=2, beta1=1.0), dict(optimizer=2, beta2=-0.5),
-               dict(optimizer=2, eps=-1.0), dict(optimizer=2, eps=float("inf"))]:
+               dict(optimizer=2, eps=-1.0), dict(optimizer=2, eps=float("inf")),
+               dict(workgroups=-1)]:
         a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
                  weight_decay=1e-4, nesterov=True, schedule=None, resident_bytes=None,
                  key_group=None, num_groups=None, unfused=False, optimizer=None, beta1=0.9,
-                 beta2=0.999, eps=1e-8)
+                 beta2=0.999, eps=1e-8, workgroups=None)
         a.update(kw)
         rc, h = lib.phub_init(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["lr"],
                               a["momentum"], a["weight_decay"], a["nesterov"], check=False,
                               schedule=a["schedule"], resident_bytes=a["resident_bytes"],
                               key_group=a["key_group"], num_groups=a["num_groups"],
                               unfused=a["unfused"], optimizer=a["optimizer"], beta1=a["beta1"],
-                              beta2=a["beta2"], eps=a["eps"])
+                              beta2=a["beta2"], eps=a["eps"], workgroups=a["workgroups"])
         assert rc == phub.PHUB_EINVAL and h is None, kw
 
 
