@@ -61,7 +61,8 @@ typedef struct phub_job phub_job;
  *   num_workers   N, 1 <= N <= 4096: the number of gradients summed per key.
  *   num_keys      K >= 1: the number of keys (one layer's parameters each,
  *                 section 2).
- *   key_elems     host array of K element counts, each 0 <= n_k < 2^40.
+ *   key_elems     host array of K element counts, each 0 <= n_k < 2^34
+ *                 (the schedule functions below accept up to 2^40).
  *   chunk_bytes   size of the chunks keys are split into for scheduling
  *                 (section 3.2.3; the paper's default is 32768); a positive
  *                 multiple of 16, at most 2^30.  Results do not depend on it.
@@ -137,8 +138,8 @@ typedef struct phub_options {
                                other optimizers; momentum and nesterov of
                                phub_init_ex are ignored by SGD and Adam. */
     int workgroups;         /* persistent workgroups of the job's launch (each
-                               a wave per SIMD of one compute unit); 0: one
-                               per compute unit.  Fewer let concurrent
+                               a wave per SIMD of one compute unit), at most
+                               65536; 0: one per compute unit.  Fewer let concurrent
                                tenants share the chip without each keeping a
                                full grid of loads in flight. */
     int unfused;            /* ablation of the fused pass (section 3.2.2:

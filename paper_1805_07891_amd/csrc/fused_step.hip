@@ -225,7 +225,7 @@ struct TileStreams {
 template <int NW, int S>
 __device__ __forceinline__ void tile_bases(TileStreams<NW, S>& s, const DevTile& d,
                                            float* const* state) {
-    const uint32_t vlo = uint32_t(d.vec) & kVecLowMask;
+    const uint32_t vlo = d.vec & kVecLowMask;
 #pragma unroll
     for (int i = 0; i < S; ++i) s.st[i] = state[i] + d.arena_offset - size_t(vlo) * 4;
     s.off = (vlo + (threadIdx.x & 63u)) * 16u;
@@ -235,7 +235,7 @@ __device__ __forceinline__ void tile_bases(TileStreams<NW, S>& s, const DevTile&
 template <int NW, int S>
 __device__ __forceinline__ void tile_streams(TileStreams<NW, S>& s, const DevTile& d,
                                              const float* const* row, float* const* state) {
-    const uint32_t vhi = uint32_t(d.vec) & ~kVecLowMask;
+    const uint32_t vhi = d.vec & ~kVecLowMask;
 #pragma unroll
     for (int w = 0; w < NW; ++w) s.g[w] = row[w] + size_t(vhi) * 4;
     s.vhi = vhi;
@@ -263,7 +263,7 @@ __device__ __forceinline__ const float* lane_pointer(uint64_t row, int w) {
 template <int NW, int S>
 __device__ __forceinline__ void tile_streams(TileStreams<NW, S>& s, const DevTile& d,
                                              uint64_t row, float* const* state) {
-    const uint32_t vhi = uint32_t(d.vec) & ~kVecLowMask;
+    const uint32_t vhi = d.vec & ~kVecLowMask;
 #pragma unroll
     for (int w = 0; w < NW; ++w) s.g[w] = lane_pointer(row, w) + size_t(vhi) * 4;
     s.vhi = vhi;

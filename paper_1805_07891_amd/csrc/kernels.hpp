@@ -23,12 +23,16 @@ static_assert(kBlockThreads >= 64 && kBlockThreads <= 1024 && kBlockThreads % 64
 constexpr int kVecPerLane = 4;
 constexpr int64_t kTileElems = 64 * 4 * kVecPerLane;
 
+// Largest key the device descriptors address: a tile's float4 index is 32
+// bits.
+constexpr int64_t kMaxDeviceKeyElems = int64_t(1) << 34;
+
 // One full tile (16 bytes): kTileElems elements of a key starting at
-// element 4 * vec.
+// element 4 * vec (keys therefore hold fewer than kMaxDeviceKeyElems).
 struct DevTile {
     int64_t arena_offset;  // index of the tile's first element in the W and M arenas
     int32_t key;           // the key's row in the gradient pointer table
-    int32_t vec;           // index of the tile's first float4 within the key
+    uint32_t vec;          // index of the tile's first float4 within the key
 };
 static_assert(sizeof(DevTile) == 16, "DevTile layout");
 

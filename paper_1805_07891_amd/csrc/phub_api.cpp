@@ -62,6 +62,7 @@ constexpr int kLptItemsPerBin = PHUB_LPT_ITEMS_PER_BIN;
 namespace {
 
 constexpr int kStageSlots = 4;       // pinned staging buffers for pointer-table uploads
+constexpr int kMaxWorkgroups = 1 << 16;  // largest persistent grid a job may ask for
 constexpr int64_t kArenaAlign = 64;  // elements: 256-byte aligned key slices
 
 thread_local std::string g_error;
@@ -459,6 +460,10 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         std::string err = phub::validate_shape(num_workers, num_keys, key_elems, chunk_bytes);
         if (!err.empty()) return fail(PHUB_EINVAL, "%s", err.c_str());
     }
+    for (int k = 0; k < num_keys; ++k)
+        if (key_elems[k] >= phub::kMaxDeviceKeyElems)
+            return fail(PHUB_EINVAL, "key_elems[%d] = %lld exceeds the %lld elements a key may hold",
+                        k, (long long)key_elems[k], (long long)(phub::kMaxDeviceKeyElems - 1));
     if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
         return fail(PHUB_EINVAL, "lr, momentum and weight_decay must be finite");
     int schedule = phub::kScheduleLpt;
@@ -469,8 +474,9 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     float beta1 = 0, beta2 = 0, eps = 0;
     int workgroups = 0;  // 0: one per compute unit
     if (options) {
-        if (options->workgroups < 0)
-            return fail(PHUB_EINVAL, "workgroups must be >= 0, got %d", options->workgroups);
+        if (options->workgroups < 0 || options->workgroups > kMaxWorkgroups)
+            return fail(PHUB_EINVAL, "workgroups must be in [0, %d], got %d", kMaxWorkgroups,
+                        options->workgroups);
         workgroups = options->workgroups;
         if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
@@ -676,7 +682,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                     const int64_t nfull = sg.count / phub::kTileElems;
                     for (int64_t t = 0; t < nfull; ++t)
                         dtiles.push_back({ao + t * phub::kTileElems, row,
-                                          int32_t((sg.offset + t * phub::kTileElems) / 4)});
+                                          uint32_t((sg.offset + t * phub::kTileElems) / 4)});
                     const int64_t done = nfull * phub::kTileElems;
                     if (done < sg.count)
                         drems.push_back({ao + done, sg.offset + done, row,

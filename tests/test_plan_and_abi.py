@@ -246,7 +246,7 @@ def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
                dict(key_group=[0, 1], unfused=True), dict(optimizer=7),
                dict(optimizer=2, beta1=1.0), dict(optimizer=2, beta2=-0.5),
                dict(optimizer=2, eps=-1.0), dict(optimizer=2, eps=float("inf")),
-               dict(workgroups=-1)]:
+               dict(workgroups=-1), dict(workgroups=1 << 17), dict(key_elems=[4, 1 << 34])]:
         a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
                  weight_decay=1e-4, nesterov=True, schedule=None, resident_bytes=None,
                  key_group=None, num_groups=None, unfused=False, optimizer=None, beta1=0.9,
