@@ -462,8 +462,8 @@ def main(argv=None) -> int:
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
     traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum")
                else measured_traffic(args.workload))
-    groups, threads, segs, _ = jobs[dom].info()
-    cache_resident = [job.info()[3] for job in jobs]
+    groups, threads, segs, _, _ = jobs[dom].info()
+    cached = [job.cached_fraction() for job in jobs]
 
     ceiling = read_ceiling(torch, dev, grads[dom])
 
@@ -487,8 +487,8 @@ def main(argv=None) -> int:
         "config": {
             "workload": args.workload,
             "jobs": [{"name": j.name, "workers": j.num_workers, "keys": j.num_keys,
-                      "params": j.num_params, "wm_cache_resident": bool(r)}
-                     for j, r in zip(wl.jobs, cache_resident)],
+                      "params": j.num_params, "state_cached_fraction": round(r, 4)}
+                     for j, r in zip(wl.jobs, cached)],
             "chunk_bytes": args.chunk_bytes or wl.jobs[0].chunk_bytes,
             "schedule": args.schedule,
             "optimizer": ({"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,

@@ -104,19 +104,24 @@ enum phub_optimizer {
 /* Optional settings of phub_init_ex. */
 typedef struct phub_options {
     int schedule;           /* a phub_schedule value */
-    int64_t resident_bytes; /* cache budget in bytes for this job's W and M
-                               (the paper's cached model, section 4.5): when
-                               W plus M (8 bytes per padded element) fit in
-                               it, they are read and written with the
-                               cache-allocating policy so that they can stay
-                               in the GPU's memory-side cache between steps;
-                               otherwise, and for 0, they stream
-                               non-temporally like the gradients.  -1: the
-                               default, a per-device budget of 256 MiB (the
-                               memory-side cache of MI355X) shared first come,
-                               first served by the live jobs created with -1
-                               and given back by phub_destroy.  Results do
-                               not depend on it. */
+    int64_t resident_bytes; /* cache budget in bytes for this job's optimizer
+                               state (the paper's cached model, section 4.5).
+                               The state of the arena's first
+                               floor(budget / (4 S)) elements (S state arrays,
+                               4 bytes each), cut back to a tile boundary
+                               (1024 elements) inside the key that crosses
+                               that point, is read and written with the
+                               cache-allocating policy so that it can stay in
+                               the GPU's memory-side cache between steps; the
+                               rest streams non-temporally like the
+                               gradients.  0: nothing is cached; a budget at
+                               least the state's size caches all of it.  -1:
+                               the default, a per-device budget of 256 MiB
+                               (the memory-side cache of MI355X) shared first
+                               come, first served by the live jobs created
+                               with -1 (each takes what its state needs of
+                               what is left) and given back by phub_destroy.
+                               Results do not depend on it. */
     int num_groups;         /* readiness groups (sections 3.2.2-3.2.3: a
                                chunk is aggregated as soon as all of its
                                pieces have arrived).  0: none; the whole step
@@ -302,12 +307,14 @@ int phub_get_stream(phub_job *job, void **hip_stream);
 /*
  * phub_job_info - launch shape of the job's step: the number of workgroups
  * of one launch (0 if every key is empty), the threads per workgroup, the
- * number of work segments in the schedule, and 1 if W and M use the
- * cache-allocating policy (0 if they stream non-temporally).  Any output
- * may be NULL.
+ * number of work segments in the schedule, the bytes of optimizer state
+ * (S arrays over the padded arena), and how many of those bytes are
+ * scheduled as cache-resident (0: all of the state streams non-temporally;
+ * equal to the state bytes, less the padding, when all of it is cached).
+ * Any output may be NULL.
  */
 int phub_job_info(phub_job *job, int *workgroups, int *threads_per_group, int64_t *segments,
-                  int *cache_resident);
+                  int64_t *state_bytes, int64_t *resident_bytes);
 
 /*
  * phub_destroy - wait for the job's work, free its memory (W, M, schedule,

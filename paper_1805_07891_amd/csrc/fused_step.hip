@@ -28,9 +28,10 @@
 // window that continues into the wave's next tile (see the load window
 // below); each piece is optimized and written back as soon as its last
 // gradient is in.  Gradients are read once per step and loaded
-// non-temporally.  The state is read and written non-temporally, unless the
-// job keeps it in the memory-side cache between steps (RES: cache-
-// allocating policy for every state access of the launch).
+// non-temporally.  A wave has two bins: the part of the job whose state is
+// read and written non-temporally like the gradients, and the part whose
+// state stays in the memory-side cache between steps (cache-allocating
+// loads and stores).  Either may be empty.
 //
 // Arithmetic (no MFMA: the work is elementwise and HBM-bound): the sum is a
 // left fold in ascending worker index, plain fp32 additions; then the
@@ -433,56 +434,53 @@ __device__ __forceinline__ void partial(const float* const* g, float* const* stb
 
 // ---------------------------------------------------------------- kernels
 
-// NW > 0: exactly NW workers.  Each wave first streams its full tiles
-// through the load window, then its remainders.  At the start of tile t the
-// wave fetches the pointer row of tile t + 1 (one vector load), whose
-// descriptor it fetched at the start of tile t - 1, and the descriptor of
-// tile t + 2 (a scalar load); both have long arrived when the window
-// reaches tile t + 1.
-//
-// One wave per SIMD (one workgroup of 4 waves per CU).
-#define PHUB_ONE_WAVE_PER_SIMD __attribute__((amdgpu_waves_per_eu(1, 1)))
-
+// The full tiles [tb, te) of one bin, NW workers, state policy RES.  At
+// the start of tile t the wave fetches the pointer row of tile t + 1 (one
+// vector load), whose descriptor it fetched at the start of tile t - 1, and
+// the descriptor of tile t + 2 (a scalar load); both have long arrived when
+// the window reaches tile t + 1.
 template <int NW, int OPT, bool RES, bool PULL>
-__global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_step_fixed(
-    PHUB_KERNEL_ARGS) {
+__device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, int32_t tb,
+                                           int32_t te, const float* const* __restrict__ grads,
+                                           float* const* __restrict__ outs, float* const* state,
+                                           const OptArgs& o) {
     constexpr int S = kStates<OPT>;
     static_assert(kTileLoads<NW, S> % kRing<NW, S, RES> == 0,
                   "the load window must wrap with the tile");
-    float* const state[3] = {weights, moments, second};
-    const uint32_t wave = wave_index();
-
-    const int32_t tb = tile_begin[wave];
-    const int32_t te = tile_begin[wave + 1];
-    if (tb < te) {
-        const int32_t last = te - 1;
-        TilePipe<NW, S, RES> p;
-        TileStreams<NW, S> a, b;
-        uint64_t prow = 0;  // pushpull: model-buffer pointer row of the current tile
-        {
-            const DevTile first = tiles[tb];
-            tile_streams<NW, S>(a, first, grads + int64_t(first.key) * NW, state);
-            if constexpr (PULL) prow = load_row<NW>(outs + int64_t(first.key) * NW);
-        }
-        DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
-        tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
-        for (int32_t t = tb;; ++t) {
-            const bool has_next = t < last;
-            const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
-            uint64_t nprow = 0;
-            if constexpr (PULL) nprow = load_row<NW>(outs + int64_t(nd.key) * NW);
-            const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
-            tile_steps<NW, OPT, RES, PULL>(std::make_integer_sequence<int, kTileLoads<NW, S>>{},
-                                           p, a, b, nd, nrow, prow, has_next, state, o);
-            if (!has_next) break;
-            a = b;
-            nd = nd2;
-            prow = nprow;
-        }
+    if (tb >= te) return;
+    const int32_t last = te - 1;
+    TilePipe<NW, S, RES> p;
+    TileStreams<NW, S> a, b;
+    uint64_t prow = 0;  // pushpull: model-buffer pointer row of the current tile
+    {
+        const DevTile first = tiles[tb];
+        tile_streams<NW, S>(a, first, grads + int64_t(first.key) * NW, state);
+        if constexpr (PULL) prow = load_row<NW>(outs + int64_t(first.key) * NW);
     }
+    DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
+    tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
+    for (int32_t t = tb;; ++t) {
+        const bool has_next = t < last;
+        const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
+        uint64_t nprow = 0;
+        if constexpr (PULL) nprow = load_row<NW>(outs + int64_t(nd.key) * NW);
+        const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
+        tile_steps<NW, OPT, RES, PULL>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
+                                       a, b, nd, nrow, prow, has_next, state, o);
+        if (!has_next) break;
+        a = b;
+        nd = nd2;
+        prow = nprow;
+    }
+}
 
-    const int32_t rb = rem_begin[wave];
-    const int32_t re = rem_begin[wave + 1];
+// The remainders [rb, re) of one bin.
+template <int NW, int OPT, bool RES, bool PULL>
+__device__ __forceinline__ void walk_rems(const DevRem* __restrict__ rems, int32_t rb, int32_t re,
+                                          const float* const* __restrict__ grads,
+                                          float* const* __restrict__ outs, float* const* state,
+                                          const OptArgs& o) {
+    constexpr int S = kStates<OPT>;
     for (int32_t r = rb; r < re; ++r) {
         const DevRem rm = rems[r];
         const float* g[NW];
@@ -498,6 +496,30 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
         partial<NW, OPT, RES, PULL>(g, stb, out, uint32_t(rm.count) >> 2,
                                     uint32_t(rm.count) & 3u, o);
     }
+}
+
+// NW > 0: exactly NW workers.  Each wave streams the full tiles of its
+// streamed bin, then those of its cache-resident bin, then the remainders
+// of both.  All waves thus work in the same phase at almost every moment:
+// on MI355X that measured better than mixing the two kinds of traffic
+// (odd waves in the other order), and slightly better than the resident
+// bin first.  One wave per SIMD (one workgroup of 4 waves per CU).
+#define PHUB_ONE_WAVE_PER_SIMD __attribute__((amdgpu_waves_per_eu(1, 1)))
+
+template <int NW, int OPT, bool PULL>
+__global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_step_fixed(
+    PHUB_KERNEL_ARGS) {
+    float* const state[3] = {weights, moments, second};
+    const uint32_t wave = wave_index();
+    const uint32_t bins = gridDim.x * kWavesPerBlock;
+    walk_tiles<NW, OPT, false, PULL>(tiles, tile_begin[bins + wave], tile_begin[bins + wave + 1],
+                                     grads, outs, state, o);
+    walk_tiles<NW, OPT, true, PULL>(tiles, tile_begin[wave], tile_begin[wave + 1], grads, outs,
+                                    state, o);
+    walk_rems<NW, OPT, true, PULL>(rems, rem_begin[wave], rem_begin[wave + 1], grads, outs, state,
+                                   o);
+    walk_rems<NW, OPT, false, PULL>(rems, rem_begin[bins + wave], rem_begin[bins + wave + 1], grads,
+                                    outs, state, o);
 }
 
 // Any N: workers taken in batches of kBatch, each batch's loads in flight
@@ -552,14 +574,14 @@ __device__ __forceinline__ void run_any(const float* const* kp, float* const* ko
     }
 }
 
+// One bin of the any-N kernel: full tiles [tb, te), then remainders [rb, re).
 template <int OPT, bool RES, bool PULL>
-__global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS) {
+__device__ __forceinline__ void any_bin(const DevTile* __restrict__ tiles, int32_t tb, int32_t te,
+                                        const DevRem* __restrict__ rems, int32_t rb, int32_t re,
+                                        const float* const* __restrict__ grads,
+                                        float* const* __restrict__ outs, float* const* state,
+                                        int n, const OptArgs& o) {
     constexpr int S = kStates<OPT>;
-    float* const state[3] = {weights, moments, second};
-    const uint32_t wave = wave_index();
-    const int n = num_workers;
-    const int32_t tb = tile_begin[wave];
-    const int32_t te = tile_begin[wave + 1];
     for (int32_t t = tb; t < te; ++t) {
         const DevTile tl = tiles[t];
         float* stb[S];
@@ -569,8 +591,6 @@ __global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS
                                 PULL ? outs + int64_t(tl.key) * n : nullptr, n,
                                 int64_t(tl.vec) * 4, stb, uint32_t(kTileElems / 4), 0u, o);
     }
-    const int32_t rb = rem_begin[wave];
-    const int32_t re = rem_begin[wave + 1];
     for (int32_t r = rb; r < re; ++r) {
         const DevRem rm = rems[r];
         float* stb[S];
@@ -580,6 +600,18 @@ __global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS
                                 PULL ? outs + int64_t(rm.key) * n : nullptr, n, rm.offset, stb,
                                 uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u, o);
     }
+}
+
+template <int OPT, bool PULL>
+__global__ __launch_bounds__(kBlockThreads) void fused_step_any(PHUB_KERNEL_ARGS) {
+    float* const state[3] = {weights, moments, second};
+    const uint32_t wave = wave_index();
+    const uint32_t bins = gridDim.x * kWavesPerBlock;
+    any_bin<OPT, false, PULL>(tiles, tile_begin[bins + wave], tile_begin[bins + wave + 1], rems,
+                              rem_begin[bins + wave], rem_begin[bins + wave + 1], grads, outs,
+                              state, num_workers, o);
+    any_bin<OPT, true, PULL>(tiles, tile_begin[wave], tile_begin[wave + 1], rems, rem_begin[wave],
+                             rem_begin[wave + 1], grads, outs, state, num_workers, o);
 }
 
 // Ablation: the unfused ("wide") form of the step, kept to measure what
@@ -629,32 +661,36 @@ __device__ __forceinline__ void optimize_range(const float* sum, float* const* s
 
 __global__ __launch_bounds__(kBlockThreads) void aggregate_only(PHUB_KERNEL_ARGS, float* merge) {
     const uint32_t wave = wave_index();
+    const uint32_t bins = gridDim.x * kWavesPerBlock;
     const int n = num_workers;
-    for (int32_t t = tile_begin[wave]; t < tile_begin[wave + 1]; ++t) {
-        const DevTile tl = tiles[t];
-        aggregate_range(grads + int64_t(tl.key) * n, n, int64_t(tl.vec) * 4,
-                        merge + tl.arena_offset, uint32_t(kTileElems / 4), 0u);
-    }
-    for (int32_t r = rem_begin[wave]; r < rem_begin[wave + 1]; ++r) {
-        const DevRem rm = rems[r];
-        aggregate_range(grads + int64_t(rm.key) * n, n, rm.offset, merge + rm.arena_offset,
-                        uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u);
+    for (uint32_t bin : {wave, bins + wave}) {
+        for (int32_t t = tile_begin[bin]; t < tile_begin[bin + 1]; ++t) {
+            const DevTile tl = tiles[t];
+            aggregate_range(grads + int64_t(tl.key) * n, n, int64_t(tl.vec) * 4,
+                            merge + tl.arena_offset, uint32_t(kTileElems / 4), 0u);
+        }
+        for (int32_t r = rem_begin[bin]; r < rem_begin[bin + 1]; ++r) {
+            const DevRem rm = rems[r];
+            aggregate_range(grads + int64_t(rm.key) * n, n, rm.offset, merge + rm.arena_offset,
+                            uint32_t(rm.count) >> 2, uint32_t(rm.count) & 3u);
+        }
     }
 }
 
 template <int OPT, bool RES>
-__global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS, float* merge) {
+__device__ __forceinline__ void optimize_bin(const DevTile* __restrict__ tiles, int32_t tb,
+                                             int32_t te, const DevRem* __restrict__ rems,
+                                             int32_t rb, int32_t re, const float* merge,
+                                             float* const* state, const OptArgs& o) {
     constexpr int S = kStates<OPT>;
-    float* const state[3] = {weights, moments, second};
-    const uint32_t wave = wave_index();
-    for (int32_t t = tile_begin[wave]; t < tile_begin[wave + 1]; ++t) {
+    for (int32_t t = tb; t < te; ++t) {
         const DevTile tl = tiles[t];
         float* stb[S];
 #pragma unroll
         for (int i = 0; i < S; ++i) stb[i] = state[i] + tl.arena_offset;
         optimize_range<OPT, RES>(merge + tl.arena_offset, stb, uint32_t(kTileElems / 4), 0u, o);
     }
-    for (int32_t r = rem_begin[wave]; r < rem_begin[wave + 1]; ++r) {
+    for (int32_t r = rb; r < re; ++r) {
         const DevRem rm = rems[r];
         float* stb[S];
 #pragma unroll
@@ -664,88 +700,91 @@ __global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS,
     }
 }
 
+template <int OPT>
+__global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS, float* merge) {
+    float* const state[3] = {weights, moments, second};
+    const uint32_t wave = wave_index();
+    const uint32_t bins = gridDim.x * kWavesPerBlock;
+    optimize_bin<OPT, true>(tiles, tile_begin[wave], tile_begin[wave + 1], rems, rem_begin[wave],
+                            rem_begin[wave + 1], merge, state, o);
+    optimize_bin<OPT, false>(tiles, tile_begin[bins + wave], tile_begin[bins + wave + 1], rems,
+                             rem_begin[bins + wave], rem_begin[bins + wave + 1], merge, state, o);
+}
+
 // -------------------------------------------------------------- launchers
 
 #define PHUB_LAUNCH_ARGS                                                                     \
     p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.outs, p.weights, p.moments,        \
         p.second, p.opt, p.num_workers
 
-template <int OPT, bool RES, bool PULL>
+template <int OPT, bool PULL>
 hipError_t launch_any(const StepParams& p, int grid, hipStream_t stream) {
-    hipLaunchKernelGGL((fused_step_any<OPT, RES, PULL>), dim3(grid), dim3(kBlockThreads), 0,
-                       stream, PHUB_LAUNCH_ARGS);
+    hipLaunchKernelGGL((fused_step_any<OPT, PULL>), dim3(grid), dim3(kBlockThreads), 0, stream,
+                       PHUB_LAUNCH_ARGS);
     return hipGetLastError();
 }
 
-template <int NW, int OPT, bool RES, bool PULL>
+template <int NW, int OPT, bool PULL>
 hipError_t launch_one(const StepParams& p, int grid, hipStream_t stream) {
     constexpr int S = kStates<OPT>;
-    if constexpr (kTileLoads<NW, S> % kRing<NW, S, RES> == 0) {
-        hipLaunchKernelGGL((fused_step_fixed<NW, OPT, RES, PULL>), dim3(grid),
-                           dim3(kBlockThreads), 0, stream, PHUB_LAUNCH_ARGS);
+    if constexpr (kTileLoads<NW, S> % kRing<NW, S, true> == 0 &&
+                  kTileLoads<NW, S> % kRing<NW, S, false> == 0) {
+        hipLaunchKernelGGL((fused_step_fixed<NW, OPT, PULL>), dim3(grid), dim3(kBlockThreads), 0,
+                           stream, PHUB_LAUNCH_ARGS);
         return hipGetLastError();
     } else {
-        return launch_any<OPT, RES, PULL>(p, grid, stream);
+        return launch_any<OPT, PULL>(p, grid, stream);
     }
 }
 
-template <int OPT, bool RES, bool PULL>
+template <int OPT, bool PULL>
 hipError_t launch_pull(const StepParams& p, int grid, hipStream_t stream) {
     switch (p.num_workers) {
-        case 1: return launch_one<1, OPT, RES, PULL>(p, grid, stream);
-        case 2: return launch_one<2, OPT, RES, PULL>(p, grid, stream);
-        case 3: return launch_one<3, OPT, RES, PULL>(p, grid, stream);
-        case 4: return launch_one<4, OPT, RES, PULL>(p, grid, stream);
-        case 5: return launch_one<5, OPT, RES, PULL>(p, grid, stream);
-        case 6: return launch_one<6, OPT, RES, PULL>(p, grid, stream);
-        case 7: return launch_one<7, OPT, RES, PULL>(p, grid, stream);
-        case 8: return launch_one<8, OPT, RES, PULL>(p, grid, stream);
-        case 9: return launch_one<9, OPT, RES, PULL>(p, grid, stream);
-        case 10: return launch_one<10, OPT, RES, PULL>(p, grid, stream);
-        case 11: return launch_one<11, OPT, RES, PULL>(p, grid, stream);
-        case 12: return launch_one<12, OPT, RES, PULL>(p, grid, stream);
-        case 13: return launch_one<13, OPT, RES, PULL>(p, grid, stream);
-        case 14: return launch_one<14, OPT, RES, PULL>(p, grid, stream);
-        case 15: return launch_one<15, OPT, RES, PULL>(p, grid, stream);
-        case 16: return launch_one<16, OPT, RES, PULL>(p, grid, stream);
-        default: return launch_any<OPT, RES, PULL>(p, grid, stream);
+        case 1: return launch_one<1, OPT, PULL>(p, grid, stream);
+        case 2: return launch_one<2, OPT, PULL>(p, grid, stream);
+        case 3: return launch_one<3, OPT, PULL>(p, grid, stream);
+        case 4: return launch_one<4, OPT, PULL>(p, grid, stream);
+        case 5: return launch_one<5, OPT, PULL>(p, grid, stream);
+        case 6: return launch_one<6, OPT, PULL>(p, grid, stream);
+        case 7: return launch_one<7, OPT, PULL>(p, grid, stream);
+        case 8: return launch_one<8, OPT, PULL>(p, grid, stream);
+        case 9: return launch_one<9, OPT, PULL>(p, grid, stream);
+        case 10: return launch_one<10, OPT, PULL>(p, grid, stream);
+        case 11: return launch_one<11, OPT, PULL>(p, grid, stream);
+        case 12: return launch_one<12, OPT, PULL>(p, grid, stream);
+        case 13: return launch_one<13, OPT, PULL>(p, grid, stream);
+        case 14: return launch_one<14, OPT, PULL>(p, grid, stream);
+        case 15: return launch_one<15, OPT, PULL>(p, grid, stream);
+        case 16: return launch_one<16, OPT, PULL>(p, grid, stream);
+        default: return launch_any<OPT, PULL>(p, grid, stream);
     }
 }
 
-template <int OPT, bool RES>
-hipError_t launch_fused(const StepParams& p, int grid, hipStream_t stream) {
-    return p.outs ? launch_pull<OPT, RES, true>(p, grid, stream)
-                  : launch_pull<OPT, RES, false>(p, grid, stream);
-}
-
-template <int OPT, bool RES>
+template <int OPT>
 hipError_t launch_unfused(const StepParams& p, int grid, hipStream_t stream) {
     hipLaunchKernelGGL(aggregate_only, dim3(grid), dim3(kBlockThreads), 0, stream,
                        PHUB_LAUNCH_ARGS, p.merge);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-    hipLaunchKernelGGL((optimize_only<OPT, RES>), dim3(grid), dim3(kBlockThreads), 0, stream,
+    hipLaunchKernelGGL((optimize_only<OPT>), dim3(grid), dim3(kBlockThreads), 0, stream,
                        PHUB_LAUNCH_ARGS, p.merge);
     return hipGetLastError();
 }
 
 template <int OPT>
-hipError_t launch_opt(const StepParams& p, bool resident, int grid, hipStream_t stream) {
-    if (p.merge)
-        return resident ? launch_unfused<OPT, true>(p, grid, stream)
-                        : launch_unfused<OPT, false>(p, grid, stream);
-    return resident ? launch_fused<OPT, true>(p, grid, stream)
-                    : launch_fused<OPT, false>(p, grid, stream);
+hipError_t launch_opt(const StepParams& p, int grid, hipStream_t stream) {
+    if (p.merge) return launch_unfused<OPT>(p, grid, stream);
+    return p.outs ? launch_pull<OPT, true>(p, grid, stream)
+                  : launch_pull<OPT, false>(p, grid, stream);
 }
 
 }  // namespace
 
-hipError_t launch_fused_step(const StepParams& p, int optimizer, bool resident, int grid,
-                             hipStream_t stream) {
+hipError_t launch_fused_step(const StepParams& p, int optimizer, int grid, hipStream_t stream) {
     switch (optimizer) {
-        case kOptMomentum: return launch_opt<kOptMomentum>(p, resident, grid, stream);
-        case kOptNesterov: return launch_opt<kOptNesterov>(p, resident, grid, stream);
-        case kOptSgd: return launch_opt<kOptSgd>(p, resident, grid, stream);
-        case kOptAdam: return launch_opt<kOptAdam>(p, resident, grid, stream);
+        case kOptMomentum: return launch_opt<kOptMomentum>(p, grid, stream);
+        case kOptNesterov: return launch_opt<kOptNesterov>(p, grid, stream);
+        case kOptSgd: return launch_opt<kOptSgd>(p, grid, stream);
+        case kOptAdam: return launch_opt<kOptAdam>(p, grid, stream);
         default: return hipErrorInvalidValue;
     }
 }

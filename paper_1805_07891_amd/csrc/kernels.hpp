@@ -65,11 +65,18 @@ struct OptArgs {
     float b1, b2, c1, c2, k1, k2, eps;
 };
 
+// The schedule of one launch has two bins per wave.  With
+// bins = grid * kBlockThreads / 64 waves, the bin tables hold 2 * bins + 1
+// offsets: wave w's cache-resident bin is [begin[w], begin[w+1]) (its state
+// stays in the memory-side cache between steps: cache-allocating loads and
+// stores), its streamed bin [begin[bins+w], begin[bins+w+1]) (state read
+// and written non-temporally).  The fused kernels walk the streamed bin
+// first.
 struct StepParams {
-    const DevTile* tiles;         // grouped by bin (one bin per wave)
-    const int32_t* tile_begin;    // wave w owns tiles [tile_begin[w], tile_begin[w+1])
+    const DevTile* tiles;         // grouped by bin
+    const int32_t* tile_begin;    // 2 * bins + 1 offsets into tiles
     const DevRem* rems;           // grouped by bin
-    const int32_t* rem_begin;     // wave w owns rems [rem_begin[w], rem_begin[w+1])
+    const int32_t* rem_begin;     // 2 * bins + 1 offsets into rems
     const float* const* grads;    // [row * num_workers + worker], 16-byte aligned
     float* const* outs;           // same layout: model buffers that receive w' (pushpull), or null
     float* merge;                 // unfused ablation: sum buffer laid out like W, or null (fused)
@@ -84,10 +91,7 @@ struct StepParams {
 // (and, when p.outs is set, writes the updated weights into every worker's
 // model buffer in the same pass; when p.merge is set, runs the unfused
 // two-pass ablation instead): `grid` workgroups of kBlockThreads threads,
-// one bin per wave (the bin tables have grid * kBlockThreads / 64 + 1
-// entries).  `optimizer` is an OptKind.  `resident`: the state uses the
-// cache-allocating policy instead of non-temporal accesses.
-hipError_t launch_fused_step(const StepParams& p, int optimizer, bool resident, int grid,
-                             hipStream_t stream);
+// two bins per wave as described above.  `optimizer` is an OptKind.
+hipError_t launch_fused_step(const StepParams& p, int optimizer, int grid, hipStream_t stream);
 
 }  // namespace phub

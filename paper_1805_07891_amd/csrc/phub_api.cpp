@@ -41,10 +41,11 @@
 #endif
 // Default cache budget per device, shared by the jobs created with the
 // default option: the size of MI355X's memory-side cache (256 MiB).  A job
-// whose W plus M fit in what is left of it reads and writes them with the
-// cache-allocating policy, so that they can stay in that cache between
-// steps (the paper's cached model, section 4.5); otherwise they stream
-// non-temporally like the gradients.
+// takes as much of what is left as its optimizer state needs: that part of
+// the state (a prefix of the arena) is read and written with the
+// cache-allocating policy, so that it can stay in that cache between steps
+// (the paper's cached model, section 4.5); the rest streams non-temporally
+// like the gradients.
 #ifndef PHUB_DEVICE_CACHE_BYTES
 #define PHUB_DEVICE_CACHE_BYTES (int64_t(256) << 20)
 #endif
@@ -111,8 +112,11 @@ struct phub_job {
     int64_t num_segments = 0;
     int64_t num_tiles = 0;
     int64_t num_rems = 0;
-    bool resident = false;    // W and M stay in the memory-side cache between steps
-    int64_t cache_claim = 0;  // bytes of the device's default cache budget this job holds
+    int num_states = 2;         // optimizer state arrays (W, then M and V)
+    int64_t resident_elems = 0; // arena elements [0, resident_elems) keep their state
+                                // in the memory-side cache between steps
+    int64_t resident_bytes = 0; // state bytes of the tiles actually scheduled as resident
+    int64_t cache_claim = 0;    // bytes of the device's default cache budget this job holds
 
     // Readiness groups.  Without groups the job has one group holding every
     // key, launched by phub_step.
@@ -134,7 +138,7 @@ struct phub_job {
     float* second = nullptr;   // Adam's second moment, else null
     float* merge = nullptr;  // unfused ablation only: the sum, laid out like W
     phub::DevTile* d_tiles = nullptr;
-    int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of bins + 1 entries
+    int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of 2 * bins + 1 entries
     phub::DevRem* d_rems = nullptr;
     int32_t* d_rem_begin = nullptr;   // same layout
     const float** d_grads = nullptr;  // [row * N + worker]
@@ -335,9 +339,9 @@ int launch_group(phub_job* j, int g) {
     if (j->rgroup_work[g]) {
         phub::StepParams p{};
         p.tiles = j->d_tiles;
-        p.tile_begin = j->d_tile_begin + size_t(g) * (j->bins + 1);
+        p.tile_begin = j->d_tile_begin + size_t(g) * (2 * size_t(j->bins) + 1);
         p.rems = j->d_rems;
-        p.rem_begin = j->d_rem_begin + size_t(g) * (j->bins + 1);
+        p.rem_begin = j->d_rem_begin + size_t(g) * (2 * size_t(j->bins) + 1);
         p.grads = j->d_grads;
         p.outs = pull ? j->d_outs : nullptr;
         p.merge = j->merge;
@@ -346,7 +350,7 @@ int launch_group(phub_job* j, int g) {
         p.second = j->second;
         p.opt = optimizer_args(j);
         p.num_workers = j->num_workers;
-        hipError_t e = phub::launch_fused_step(p, j->opt, j->resident, j->groups, j->stream);
+        hipError_t e = phub::launch_fused_step(p, j->opt, j->groups, j->stream);
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
     }
     j->rgroup_launched[g] = 1;
@@ -583,36 +587,82 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                                : fail(PHUB_EHIP, "device reports no compute units");
     }
 
-    // One schedule per readiness group, over the group's keys in row order.
-    std::vector<phub::Plan> plans;
+    // Cache residency: the state of arena elements [0, resident_elems) is
+    // kept in the memory-side cache.  An explicit budget is the job's own;
+    // the default takes what is left of the device's shared budget, first
+    // come first served.
+    j->num_states = j->opt == phub::kOptSgd ? 1 : j->opt == phub::kOptAdam ? 3 : 2;
+    const int64_t elem_state_bytes = j->num_states * int64_t(sizeof(float));
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        int64_t budget = resident_bytes;
+        if (budget < 0) budget = std::max<int64_t>(0, PHUB_DEVICE_CACHE_BYTES - g_cache_claimed[j->device]);
+        j->resident_elems = std::min(j->arena_elems, budget / elem_state_bytes);
+        if (resident_bytes < 0) {
+            j->cache_claim = j->resident_elems * elem_state_bytes;
+            g_cache_claimed[j->device] += j->cache_claim;
+        }
+    }
+
+    // Two schedules per readiness group over the group's keys in row order:
+    // phase 0 holds the cache-resident part of the keys, phase 1 the rest.
+    // A key that straddles resident_elems is cut at a tile boundary of the
+    // key (the part below the cut is resident), so both parts keep the
+    // 16-byte alignment of the key's start.  A part is a "virtual key": a
+    // row and a first element within the key.
+    struct VKey {
+        int row;
+        int64_t base;
+        int64_t elems;
+    };
+    std::vector<phub::Plan> plans;  // [group * 2 + phase]
+    std::vector<std::vector<VKey>> vkeys;
     {
         const int groups = workgroups > 0 ? workgroups : cus * PHUB_GROUPS_PER_CU;
         const int bins = groups * (phub::kBlockThreads / 64);
         std::string err;
         try {
-            plans.resize(j->num_rgroups);
+            plans.resize(size_t(j->num_rgroups) * 2);
+            vkeys.resize(size_t(j->num_rgroups) * 2);
             for (int g = 0; g < j->num_rgroups && err.empty(); ++g) {
-                const int r0 = j->rgroup_row_begin[g], r1 = j->rgroup_row_begin[g + 1];
-                phub::Plan& plan = plans[g];
-                if (r1 > r0) {
-                    std::vector<int64_t> elems(r1 - r0);
-                    for (int r = r0; r < r1; ++r) elems[r - r0] = key_elems[j->key_of_row[r]];
-                    err = phub::build_plan(num_workers, r1 - r0, elems.data(), chunk_bytes,
-                                           schedule, bins, kLptItemsPerBin * bins, &plan);
-                } else {
-                    plan.bin_begin.assign(1, 0);
+                for (int r = j->rgroup_row_begin[g]; r < j->rgroup_row_begin[g + 1]; ++r) {
+                    const int k = j->key_of_row[r];
+                    const int64_t n = key_elems[k], o = j->arena_offset[k];
+                    int64_t cut = 0;  // elements of the key that are resident
+                    if (o + n <= j->resident_elems)
+                        cut = n;
+                    else if (o < j->resident_elems)
+                        cut = (j->resident_elems - o) / phub::kTileElems * phub::kTileElems;
+                    if (cut > 0) vkeys[g * 2].push_back({r, 0, cut});
+                    if (cut < n || n == 0) vkeys[g * 2 + 1].push_back({r, cut, n - cut});
                 }
-                // every wave of the grid reads its bin: pad dropped bins as empty
-                while (plan.bin_begin.size() < size_t(bins) + 1)
-                    plan.bin_begin.push_back(plan.bin_begin.back());
-                j->rgroup_work[g] = plan.segments.empty() ? 0 : 1;
-                j->num_segments += int64_t(plan.segments.size());
+                for (int ph = 0; ph < 2 && err.empty(); ++ph) {
+                    const std::vector<VKey>& vk = vkeys[g * 2 + ph];
+                    phub::Plan& plan = plans[g * 2 + ph];
+                    if (!vk.empty()) {
+                        std::vector<int64_t> elems(vk.size());
+                        for (size_t i = 0; i < vk.size(); ++i) elems[i] = vk[i].elems;
+                        err = phub::build_plan(num_workers, int(vk.size()), elems.data(),
+                                               chunk_bytes, schedule, bins,
+                                               kLptItemsPerBin * bins, &plan);
+                    } else {
+                        plan.bin_begin.assign(1, 0);
+                    }
+                    // every wave of the grid reads its bins: pad dropped bins as empty
+                    while (plan.bin_begin.size() < size_t(bins) + 1)
+                        plan.bin_begin.push_back(plan.bin_begin.back());
+                    if (!plan.segments.empty()) j->rgroup_work[g] = 1;
+                    j->num_segments += int64_t(plan.segments.size());
+                }
             }
         } catch (const std::bad_alloc&) {
-            delete j;
-            return fail(PHUB_ENOMEM, "host allocation failed while building the schedule");
+            err = "host allocation failed while building the schedule";
         }
         if (!err.empty()) {
+            if (j->cache_claim) {
+                std::lock_guard<std::mutex> lk(g_live_mu);
+                g_cache_claimed[j->device] -= j->cache_claim;
+            }
             delete j;
             return fail(PHUB_EINVAL, "%s", err.c_str());
         }
@@ -620,9 +670,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->bins = bins;
     }
     j->schedule = schedule;
-    const int num_states = j->opt == phub::kOptSgd ? 1 : j->opt == phub::kOptAdam ? 3 : 2;
-    const int64_t wm_bytes = num_states * j->arena_elems * int64_t(sizeof(float));
-    if (resident_bytes >= 0) j->resident = wm_bytes > 0 && wm_bytes <= resident_bytes;
+    const int num_states = j->num_states;
 
 #define PHUB_TRY(call, what)                 \
     do {                                     \
@@ -664,36 +712,41 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         // Device form of the schedules: each bin's segments become full tiles
         // (the kernel's straight-line hot loop) and at most one remainder
         // each (partial tile and ragged end), in segment order; one block of
-        // bin offsets per readiness group.  A descriptor's key is the key's
-        // row in the pointer table.
+        // 2 * bins + 1 offsets per readiness group (the resident bins, then
+        // the streamed ones).  A descriptor's key is the key's row in the
+        // pointer table.
         std::vector<phub::DevTile> dtiles;
         std::vector<phub::DevRem> drems;
         std::vector<int32_t> tile_begin, rem_begin;
         for (int g = 0; g < j->num_rgroups; ++g) {
-            const phub::Plan& plan = plans[g];
-            const int row0 = j->rgroup_row_begin[g];
             tile_begin.push_back(int32_t(dtiles.size()));
             rem_begin.push_back(int32_t(drems.size()));
-            for (int b = 0; b < j->bins; ++b) {
-                for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
-                    const phub::PlanSegment& sg = plan.segments[i];
-                    const int row = row0 + sg.key;
-                    const int64_t ao = j->arena_offset[j->key_of_row[row]] + sg.offset;
-                    const int64_t nfull = sg.count / phub::kTileElems;
-                    for (int64_t t = 0; t < nfull; ++t)
-                        dtiles.push_back({ao + t * phub::kTileElems, row,
-                                          uint32_t((sg.offset + t * phub::kTileElems) / 4)});
-                    const int64_t done = nfull * phub::kTileElems;
-                    if (done < sg.count)
-                        drems.push_back({ao + done, sg.offset + done, row,
-                                         int32_t(sg.count - done), 0});
+            for (int ph = 0; ph < 2; ++ph) {
+                const phub::Plan& plan = plans[g * 2 + ph];
+                const std::vector<VKey>& vk = vkeys[g * 2 + ph];
+                for (int b = 0; b < j->bins; ++b) {
+                    for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
+                        const phub::PlanSegment& sg = plan.segments[i];
+                        const VKey& v = vk[sg.key];
+                        const int64_t koff = v.base + sg.offset;  // first element within the key
+                        const int64_t ao = j->arena_offset[j->key_of_row[v.row]] + koff;
+                        if (ph == 0) j->resident_bytes += int64_t(sg.count) * elem_state_bytes;
+                        const int64_t nfull = sg.count / phub::kTileElems;
+                        for (int64_t t = 0; t < nfull; ++t)
+                            dtiles.push_back({ao + t * phub::kTileElems, v.row,
+                                              uint32_t((koff + t * phub::kTileElems) / 4)});
+                        const int64_t done = nfull * phub::kTileElems;
+                        if (done < sg.count)
+                            drems.push_back({ao + done, koff + done, v.row,
+                                             int32_t(sg.count - done), 0});
+                    }
+                    if (dtiles.size() > size_t(INT32_MAX) || drems.size() > size_t(INT32_MAX)) {
+                        rc = fail(PHUB_EINVAL, "schedule too large");
+                        goto fail_cleanup;
+                    }
+                    tile_begin.push_back(int32_t(dtiles.size()));
+                    rem_begin.push_back(int32_t(drems.size()));
                 }
-                if (dtiles.size() > size_t(INT32_MAX) || drems.size() > size_t(INT32_MAX)) {
-                    rc = fail(PHUB_EINVAL, "schedule too large");
-                    goto fail_cleanup;
-                }
-                tile_begin.push_back(int32_t(dtiles.size()));
-                rem_begin.push_back(int32_t(drems.size()));
             }
         }
         j->num_tiles = int64_t(dtiles.size());
@@ -743,20 +796,16 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
 
     {
         std::lock_guard<std::mutex> lk(g_live_mu);
-        if (resident_bytes < 0 && wm_bytes > 0) {
-            int64_t& claimed = g_cache_claimed[j->device];
-            if (claimed + wm_bytes <= PHUB_DEVICE_CACHE_BYTES) {
-                claimed += wm_bytes;
-                j->cache_claim = wm_bytes;
-                j->resident = true;
-            }
-        }
         g_live.insert(j);
     }
     *out = j;
     return PHUB_OK;
 
 fail_cleanup:
+    if (j->cache_claim) {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        g_cache_claimed[j->device] -= j->cache_claim;
+    }
     release(j);
     return rc;
 }
@@ -911,12 +960,13 @@ int phub_get_stream(phub_job* j, void** hip_stream) {
 }
 
 int phub_job_info(phub_job* j, int* workgroups, int* threads_per_group, int64_t* segments,
-                  int* cache_resident) {
+                  int64_t* state_bytes, int64_t* resident_bytes) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     if (workgroups) *workgroups = j->groups;
     if (threads_per_group) *threads_per_group = phub::kBlockThreads;
     if (segments) *segments = j->num_segments;
-    if (cache_resident) *cache_resident = j->resident ? 1 : 0;
+    if (state_bytes) *state_bytes = j->num_states * j->arena_elems * int64_t(sizeof(float));
+    if (resident_bytes) *resident_bytes = j->resident_bytes;
     return PHUB_OK;
 }
 

@@ -191,7 +191,15 @@ class TorchJob:
         return [arena[o:o + n] for o, n in zip(self.offsets, self.spec.key_elems)]
 
     def info(self):
+        """(workgroups, threads per workgroup, segments, state bytes,
+        cache-resident state bytes) of the job's launch."""
         return self.lib.phub_job_info(self.handle)
+
+    def cached_fraction(self) -> float:
+        """Share of the optimizer state (unpadded) scheduled as cache-resident."""
+        states = {"momentum": 2, "sgd": 1, "adam": 3}[self.optimizer]
+        total = states * 4 * self.spec.num_params
+        return self.info()[4] / total if total else 1.0
 
     def destroy(self) -> None:
         if self.handle is not None:

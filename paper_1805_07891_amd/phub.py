@@ -89,7 +89,7 @@ class Library:
             "phub_sync": ([vp], i32),
             "phub_get_stream": ([vp, pp], i32),
             "phub_job_info": ([vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64),
-                               ctypes.POINTER(i32)], i32),
+                               ctypes.POINTER(i64), ctypes.POINTER(i64)], i32),
             "phub_destroy": ([vp], i32),
             "phub_last_error": ([], ctypes.c_char_p),
             "phub_plan_count": ([i32, i32, vp, i64, i32, i32, i32, ctypes.POINTER(i64),
@@ -229,11 +229,13 @@ class Library:
         return out.value or 0
 
     def phub_job_info(self, job):
-        """(workgroups, threads per workgroup, segments, cache_resident)."""
-        g, t, s, r = ctypes.c_int(), ctypes.c_int(), ctypes.c_int64(), ctypes.c_int()
+        """(workgroups, threads per workgroup, segments, state bytes,
+        cache-resident state bytes)."""
+        g, t, s, sb, r = (ctypes.c_int(), ctypes.c_int(), ctypes.c_int64(), ctypes.c_int64(),
+                          ctypes.c_int64())
         self._check(self.lib.phub_job_info(job, ctypes.byref(g), ctypes.byref(t), ctypes.byref(s),
-                                           ctypes.byref(r)), True)
-        return g.value, t.value, s.value, r.value
+                                           ctypes.byref(sb), ctypes.byref(r)), True)
+        return g.value, t.value, s.value, sb.value, r.value
 
     def phub_destroy(self, job, check: bool = True) -> int:
         return self._check(self.lib.phub_destroy(job), check)

@@ -95,7 +95,7 @@ KEYS = (5, 1024, 8193, 40000, 3, 70001, 2048, 131072, 1)
 
 @pytest.mark.parametrize("optimizer", ["sgd", "adam"])
 @pytest.mark.parametrize("n_workers", [1, 4, 8, 16, 17])
-@pytest.mark.parametrize("resident", [0, 1 << 40])
+@pytest.mark.parametrize("resident", [0, 12 * 50000, 1 << 40])
 def test_optimizer_matches_the_oracle(lib, torch_dev, optimizer, n_workers, resident):
     torch, dev = torch_dev
     _say(optimizer, "N", n_workers, "resident", resident)

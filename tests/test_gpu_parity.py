@@ -178,7 +178,7 @@ def test_chunk_size_does_not_change_results(lib, torch_dev):
 
 
 @pytest.mark.parametrize("schedule", [phub.PHUB_SCHEDULE_SPLIT, phub.PHUB_SCHEDULE_LPT])
-@pytest.mark.parametrize("resident", [0, 4096, 1 << 20, 1 << 40])
+@pytest.mark.parametrize("resident", [0, 4096, 1 << 20, 8 * 150001, 1 << 40])
 def test_schedule_and_cache_residency_do_not_change_results(lib, torch_dev, schedule, resident):
     torch, dev = torch_dev
     keys = [3, 100, 8192 * 3 + 5, 70000, 1, 4096, 333333]
@@ -264,30 +264,39 @@ def test_all_keys_empty(lib, torch_dev):
 
 def test_default_cache_budget_is_shared(lib, torch_dev):
     """Jobs created with the default option share a 256 MiB per-device
-    budget for cache-resident W and M, first come first served; destroying
-    a job gives its share back; an explicit budget is the job's own."""
+    budget for cache-resident optimizer state, first come first served: each
+    takes what its state needs of what is left (a prefix of its arena,
+    possibly partial); destroying a job gives its share back; an explicit
+    budget is the job's own."""
     torch, dev = torch_dev
-    elems = 75 << 18                     # W + M = 150 MiB
+    MiB = 1 << 20
+    elems = 75 << 18                     # W + M = 150 MiB, no arena padding
     spec = Job("budget", 1, (elems,))
     a = TorchJob(spec, dev, lib=lib)
     b = TorchJob(spec, dev, lib=lib)
     c = TorchJob(spec, dev, lib=lib, resident_bytes=1 << 40)
     d = TorchJob(spec, dev, lib=lib, resident_bytes=0)
+    e = None
     try:
-        assert a.info()[3] == 1
-        assert b.info()[3] == 0          # 300 MiB would exceed the budget
-        assert c.info()[3] == 1
-        assert d.info()[3] == 0
+        assert a.info()[3] == 150 * MiB and a.info()[4] == 150 * MiB
+        assert b.info()[4] == 106 * MiB  # what is left: 106 MiB = 13568 whole tiles
+        assert c.info()[4] == 150 * MiB
+        assert d.info()[4] == 0
         a.destroy()
         a = None
         e = TorchJob(spec, dev, lib=lib)
-        assert e.info()[3] == 1          # a's share came back
+        assert e.info()[4] == 150 * MiB  # a's share came back
         e.destroy()
+        e = None
         tiny = TorchJob(Job("budget.tiny", 1, (1000,)), dev, lib=lib)
-        assert tiny.info()[3] == 1
+        assert tiny.cached_fraction() == 1.0
         tiny.destroy()
+        # an explicit budget that ends inside the key: cut at a tile boundary
+        f = TorchJob(spec, dev, lib=lib, resident_bytes=8 * 5000)
+        assert f.info()[4] == 8 * 4096
+        f.destroy()
     finally:
-        for j in (a, b, c, d):
+        for j in (a, b, c, d, e):
             if j is not None:
                 j.destroy()
 

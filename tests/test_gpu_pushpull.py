@@ -92,7 +92,7 @@ KEYS = (5, 1024, 8193, 40000, 3, 70001, 2048, 131072, 1)
 
 
 @pytest.mark.parametrize("n_workers", [1, 4, 8, 16, 17])
-@pytest.mark.parametrize("resident", [0, 1 << 40])
+@pytest.mark.parametrize("resident", [0, 8 * 50000, 1 << 40])
 def test_pushpull_writes_the_updated_weights_to_every_worker(lib, torch_dev, n_workers, resident):
     torch, dev = torch_dev
     _say("pushpull N", n_workers, "resident", resident)

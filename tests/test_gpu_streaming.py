@@ -183,13 +183,16 @@ def test_missing_push_leaves_completed_groups_applied(lib, torch_dev):
     c.job.destroy()
 
 
-def test_grouped_and_plain_jobs_share_the_cache_budget_and_results(lib, torch_dev):
-    """A grouped job with cache-resident W and M (deep load window) gives the
-    same bits as the oracle too."""
+@pytest.mark.parametrize("resident", [1 << 40, 8 * 60000])
+def test_grouped_job_with_cache_resident_state(lib, torch_dev, resident):
+    """A grouped job whose state is wholly or partly cache-resident (both
+    phases of the schedule in every group's launch) gives the same bits as
+    the oracle too."""
     torch, dev = torch_dev
     c = Case(torch, dev, lib, 8, KEYS, key_group=[k % 3 for k in range(len(KEYS))], seed=14,
-             resident_bytes=1 << 40)
-    assert c.job.info()[3] == 1
+             resident_bytes=resident)
+    frac = c.job.cached_fraction()
+    assert frac == 1.0 if resident == 1 << 40 else 0.0 < frac < 1.0
     for t in range(2):
         host = c.host_grads()
         arenas = [torch.from_numpy(a).to(dev) for a in host]
@@ -199,5 +202,5 @@ def test_grouped_and_plain_jobs_share_the_cache_budget_and_results(lib, torch_de
         c.job.push_all()
         c.job.step()
         c.oracle_step(host)
-        c.check(f"resident grouped step {t}")
+        c.check(f"resident={resident} grouped step {t}")
     c.job.destroy()
