@@ -355,6 +355,10 @@ def main(argv=None) -> int:
     ap.add_argument("--producer-mb", type=float, default=8.0,
                     help="--streaming: the simulated backward writes its gradients in buckets "
                          "of this many MB per worker, one event each")
+    ap.add_argument("--own-streams", action="store_true",
+                    help="multi-job workloads: each job on its own stream, its launches "
+                         "running concurrently with the other jobs' (default: the jobs "
+                         "share one stream and take turns, each launch with the whole GPU)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 512 MiB device copy three times (a known-size "
                          "reference for hardware byte counters)")
@@ -389,9 +393,14 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         del src, dst
 
+    # Co-running jobs share one stream by default: their steps take turns,
+    # each launch with the whole GPU (measured faster than concurrent launches
+    # on separate streams, which compete for HBM and stretch each other).
+    shared_stream = len(wl.jobs) > 1 and not args.own_streams
+    one_stream = torch.cuda.Stream(device=dev)
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
-        stream = torch.cuda.Stream(device=dev)
+        stream = one_stream if shared_stream or ji == 0 else torch.cuda.Stream(device=dev)
         job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
                        chunk_bytes=args.chunk_bytes, unfused=args.unfused,
                        optimizer=None if args.optimizer == "momentum" else args.optimizer,
@@ -501,6 +510,8 @@ def main(argv=None) -> int:
             "pushpull": args.pushpull,
             "optimizer_kind": args.optimizer,
             "unfused": args.unfused,
+            "streams": ("one shared by the jobs" if shared_stream else
+                        "one per job" if len(wl.jobs) > 1 else "one"),
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},
             "host_us_per_step": round(host_s * 1e6 / K, 2),
