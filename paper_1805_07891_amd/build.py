@@ -68,6 +68,17 @@ def build_probe(out: str = PROBE_LIB, verbose: bool = False) -> str:
     return out
 
 
+def device_assembly(out: str, source: str = "fused_step.hip") -> str:
+    """Compile one HIP source of the library to gfx950 device assembly (with
+    its kernel metadata: registers, LDS, scratch, spills) at ``out``; the
+    code-generation tests read it."""
+    flags = [f for f in FLAGS if f not in ("-fPIC", "-shared")]
+    cmd = [HIPCC, *flags, f"-I{INCLUDE}", f"-I{CSRC}", "--cuda-device-only", "-S",
+           os.path.join(CSRC, source), "-o", out]
+    subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
+    return out
+
+
 def build_all(verbose: bool = False) -> None:
     build(verbose=verbose)
     build_probe(verbose=verbose)

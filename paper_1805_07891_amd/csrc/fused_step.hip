@@ -86,7 +86,7 @@ __device__ __forceinline__ float sqrt_rn(float x) {
 
 // One element: st[0] = w, st[1] = m, st[2] = v, updated in place.
 template <int OPT>
-__device__ __forceinline__ void update(float s, float* st, const OptArgs& o) {
+__device__ __forceinline__ void update(float s, float* st, OptArgs o) {
     if constexpr (OPT == kOptSgd) {
         const float d = __builtin_fmaf(o.wd, st[0], s);
         st[0] = __builtin_fmaf(o.nlr, d, st[0]);
@@ -112,7 +112,7 @@ __device__ __forceinline__ void update(float s, float* st, const OptArgs& o) {
 
 // Four elements at once (a float4 of each array).
 template <int OPT>
-__device__ __forceinline__ void update4(const f4& s, f4* st, const OptArgs& o) {
+__device__ __forceinline__ void update4(const f4& s, f4* st, OptArgs o) {
     if constexpr (OPT == kOptAdam) {
         // the square root and division per component, correctly rounded
 #pragma unroll
@@ -326,7 +326,7 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
                                           const TileStreams<NW, kStates<OPT>>& a,
                                           TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
                                           uint64_t nrow, uint64_t prow, bool has_next,
-                                          float* const* state, const OptArgs& o) {
+                                          float* const* state, OptArgs o) {
     constexpr int S = kStates<OPT>;
     constexpr int L = kTileLoads<NW, S>;
     constexpr int R = kRing<NW, S, RES>;
@@ -375,7 +375,7 @@ __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>,
                                            const TileStreams<NW, kStates<OPT>>& a,
                                            TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
                                            uint64_t nrow, uint64_t prow, bool has_next,
-                                           float* const* state, const OptArgs& o) {
+                                           float* const* state, OptArgs o) {
     (tile_step<NW, OPT, RES, PULL, I>(p, a, b, nd, nrow, prow, has_next, state, o), ...);
 }
 
@@ -393,7 +393,7 @@ __device__ __forceinline__ void tile_prologue(std::integer_sequence<int, I...>,
 template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void partial(const float* const* g, float* const* stb,
                                         float* const* out, uint32_t nvec, uint32_t rem,
-                                        const OptArgs& o) {
+                                        OptArgs o) {
     constexpr int S = kStates<OPT>;
     const uint32_t lane = threadIdx.x & 63u;
     for (uint32_t v = lane; v < nvec; v += 64u) {
@@ -443,7 +443,7 @@ template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, int32_t tb,
                                            int32_t te, const float* const* __restrict__ grads,
                                            float* const* __restrict__ outs, float* const* state,
-                                           const OptArgs& o) {
+                                           OptArgs o) {
     constexpr int S = kStates<OPT>;
     static_assert(kTileLoads<NW, S> % kRing<NW, S, RES> == 0,
                   "the load window must wrap with the tile");
@@ -479,7 +479,7 @@ template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void walk_rems(const DevRem* __restrict__ rems, int32_t rb, int32_t re,
                                           const float* const* __restrict__ grads,
                                           float* const* __restrict__ outs, float* const* state,
-                                          const OptArgs& o) {
+                                          OptArgs o) {
     constexpr int S = kStates<OPT>;
     for (int32_t r = rb; r < re; ++r) {
         const DevRem rm = rems[r];
@@ -544,7 +544,7 @@ __device__ __forceinline__ f4 sum_any(const float* const* kp, int n, int64_t off
 template <int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void run_any(const float* const* kp, float* const* ko, int n,
                                         int64_t offset, float* const* stb, uint32_t nvec,
-                                        uint32_t rem, const OptArgs& o) {
+                                        uint32_t rem, OptArgs o) {
     constexpr int S = kStates<OPT>;
     const uint32_t lane = threadIdx.x & 63u;
     for (uint32_t v = lane; v < nvec; v += 64u) {
@@ -580,7 +580,7 @@ __device__ __forceinline__ void any_bin(const DevTile* __restrict__ tiles, int32
                                         const DevRem* __restrict__ rems, int32_t rb, int32_t re,
                                         const float* const* __restrict__ grads,
                                         float* const* __restrict__ outs, float* const* state,
-                                        int n, const OptArgs& o) {
+                                        int n, OptArgs o) {
     constexpr int S = kStates<OPT>;
     for (int32_t t = tb; t < te; ++t) {
         const DevTile tl = tiles[t];
@@ -635,7 +635,7 @@ __device__ __forceinline__ void aggregate_range(const float* const* kp, int n, i
 
 template <int OPT, bool RES>
 __device__ __forceinline__ void optimize_range(const float* sum, float* const* stb, uint32_t nvec,
-                                               uint32_t rem, const OptArgs& o) {
+                                               uint32_t rem, OptArgs o) {
     constexpr int S = kStates<OPT>;
     const uint32_t lane = threadIdx.x & 63u;
     for (uint32_t v = lane; v < nvec; v += 64u) {
@@ -681,7 +681,7 @@ template <int OPT, bool RES>
 __device__ __forceinline__ void optimize_bin(const DevTile* __restrict__ tiles, int32_t tb,
                                              int32_t te, const DevRem* __restrict__ rems,
                                              int32_t rb, int32_t re, const float* merge,
-                                             float* const* state, const OptArgs& o) {
+                                             float* const* state, OptArgs o) {
     constexpr int S = kStates<OPT>;
     for (int32_t t = tb; t < te; ++t) {
         const DevTile tl = tiles[t];
