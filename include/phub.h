@@ -213,6 +213,18 @@ int phub_push_keys(phub_job *job, int worker, int count, const int *keys,
                    const float *const *grads);
 
 /*
+ * phub_push_all - every worker pushes every key in one call (section 3.1's
+ * Push, for a caller that holds all of a step's gradients): grads has
+ * num_workers * num_keys entries, grads[w * num_keys + k] being worker w's
+ * gradient for key k (host array of device pointers, read during the call
+ * only).  Same rules and errors as phub_push for each entry; either every
+ * pointer is recorded or, on an argument error (PHUB_EINVAL) or when a
+ * readiness group has already been enqueued this step (PHUB_ESTATE), none
+ * is.  With readiness groups, every group is enqueued during the call.
+ */
+int phub_push_all(phub_job *job, const float *const *grads);
+
+/*
  * phub_push_keys_event - phub_push_keys whose gradients are all ready once
  * `hip_event` has completed (as phub_push_event; NULL = ready now): one call
  * per worker for a bucket of keys that one producer event covers.  Either

@@ -889,6 +889,24 @@ int phub_push_keys_event(phub_job* j, int worker, int count, const int* keys,
     return PHUB_OK;
 }
 
+int phub_push_all(phub_job* j, const float* const* grads) {
+    if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
+    if (!grads) return fail(PHUB_EINVAL, "grads is NULL");
+    const int nk = j->num_keys;
+    for (int w = 0; w < j->num_workers; ++w)
+        for (int k = 0; k < nk; ++k)
+            if (int rc = check_grad(j, w, k, grads[size_t(w) * nk + k])) return rc;
+    if (j->streaming)
+        for (int g = 0; g < j->num_rgroups; ++g)
+            if (j->rgroup_launched[g])
+                return fail(PHUB_ESTATE,
+                            "readiness group %d was already launched this step; nothing pushed", g);
+    for (int w = 0; w < j->num_workers; ++w)
+        for (int k = 0; k < nk; ++k)
+            if (int rc = record_push(j, w, k, grads[size_t(w) * nk + k], nullptr)) return rc;
+    return PHUB_OK;
+}
+
 int phub_step(phub_job* j) {
     if (!is_live(j)) return fail(PHUB_ESTATE, "not a live job handle");
     const int64_t need = int64_t(j->num_workers) * j->num_keys;

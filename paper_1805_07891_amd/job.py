@@ -81,6 +81,8 @@ class TorchJob:
         self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers
         self._grad_refs: List = [None] * spec.num_workers
+        # every worker's key pointers in one table (worker-major) for phub_push_all
+        self._all_ptrs = (ctypes.c_void_p * (spec.num_workers * spec.num_keys))()
 
     # -- inputs ----------------------------------------------------------------
     def key_pointers(self, arena) -> List[int]:
@@ -93,7 +95,10 @@ class TorchJob:
         if arena.numel() != self.arena_elems or arena.dtype != self.torch.float32:
             raise ValueError("gradient arena has the wrong size or dtype")
         self._grad_refs[worker] = arena
-        self._ptr_arrays[worker] = _phub.pointer_array(self.key_pointers(arena))
+        ptrs = self.key_pointers(arena)
+        self._ptr_arrays[worker] = _phub.pointer_array(ptrs)
+        k = self.spec.num_keys
+        self._all_ptrs[worker * k:(worker + 1) * k] = ptrs
 
     def set_weights(self, arena) -> None:
         """Load every key's weights from a device arena (and zero M).  The
@@ -107,10 +112,11 @@ class TorchJob:
 
     # -- the step --------------------------------------------------------------
     def push_all(self) -> None:
+        """Every worker pushes every key from its attached arena (one call)."""
         for w, arr in enumerate(self._ptr_arrays):
             if arr is None:
                 raise RuntimeError(f"worker {w} has no gradient arena attached")
-            self.lib.phub_push_keys(self.handle, w, arr)
+        self.lib.phub_push_all(self.handle, self._all_ptrs)
 
     def push_key(self, worker: int, key: int, event=None) -> None:
         """Push one key of worker ``worker`` from its attached arena; with

@@ -37,7 +37,8 @@ OPTIMIZERS = {"momentum": PHUB_OPT_MOMENTUM, "sgd": PHUB_OPT_SGD, "adam": PHUB_O
 
 # Every symbol the header declares.
 EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_push_event",
-            "phub_push_keys", "phub_push_keys_event", "phub_pushpull", "phub_pushpull_keys",
+            "phub_push_keys", "phub_push_keys_event", "phub_push_all", "phub_pushpull",
+            "phub_pushpull_keys",
             "phub_step", "phub_pull", "phub_get_state", "phub_get_second_moment", "phub_sync",
             "phub_get_stream",
             "phub_job_info", "phub_destroy", "phub_last_error", "phub_plan_count",
@@ -79,6 +80,7 @@ class Library:
             "phub_push": ([vp, i32, i32, vp], i32),
             "phub_push_event": ([vp, i32, i32, vp, vp], i32),
             "phub_push_keys": ([vp, i32, i32, vp, vp], i32),
+            "phub_push_all": ([vp, vp], i32),
             "phub_push_keys_event": ([vp, i32, i32, vp, vp, vp], i32),
             "phub_pushpull": ([vp, i32, i32, vp, vp], i32),
             "phub_pushpull_keys": ([vp, i32, i32, vp, vp, vp, vp], i32),
@@ -160,6 +162,14 @@ class Library:
         """hip_event: a hipEvent_t handle as an int (torch.cuda.Event.cuda_event) or None."""
         return self._check(self.lib.phub_push_event(job, int(worker), int(key), grad_ptr, hip_event),
                            check)
+
+    def phub_push_all(self, job, grad_ptrs, check: bool = True) -> int:
+        """grad_ptrs: num_workers * num_keys device pointers, worker-major (a
+        ctypes c_void_p array, see ``pointer_array``, or a sequence of ints;
+        None is passed on as NULL)."""
+        if grad_ptrs is not None and not isinstance(grad_ptrs, ctypes.Array):
+            grad_ptrs = pointer_array(grad_ptrs)
+        return self._check(self.lib.phub_push_all(job, grad_ptrs), check)
 
     def phub_push_keys(self, job, worker: int, grad_ptrs, keys=None, check: bool = True) -> int:
         """grad_ptrs: a ctypes c_void_p array (see ``pointer_array``) or a

@@ -89,6 +89,9 @@ def run_small_case(torch, dev, lib, n_workers, key_elems, steps=2, chunk_bytes=3
         torch.cuda.synchronize()
         if push == "keys":
             job.push_all()
+        elif push == "per_worker":
+            for w in reversed(range(n_workers)):
+                lib.phub_push_keys(job.handle, w, job.key_pointers(dev_arenas[w]))
         elif push == "single_reversed":
             for k in reversed(range(spec.num_keys)):
                 for w in reversed(range(n_workers)):
@@ -195,6 +198,31 @@ def test_push_order_and_single_pushes(lib, torch_dev):
     keys = [17, 9000, 4]
     job, res = run_small_case(torch, dev, lib, 5, keys, steps=2, seed=5, push="single_reversed")
     assert_parity(res, "reversed single pushes")
+    job.destroy()
+    job, res = run_small_case(torch, dev, lib, 5, keys, steps=2, seed=5, push="per_worker")
+    assert_parity(res, "one batched push per worker")
+    job.destroy()
+
+
+def test_push_all_checks_every_pointer_before_recording(lib, torch_dev):
+    """phub_push_all validates all N * K entries first: a bad entry anywhere
+    leaves nothing recorded, so the step is refused; a good table then
+    steps."""
+    torch, dev = torch_dev
+    keys = (300, 1024, 5)
+    spec = Job("pushall", 3, keys)
+    job = TorchJob(spec, dev, lib=lib)
+    arenas = [torch.zeros(job.arena_elems, device=dev) for _ in range(3)]
+    table = [p for a in arenas for p in job.key_pointers(a)]
+    bad = list(table)
+    bad[-1] = table[-1] + 4                      # last entry misaligned
+    assert lib.phub_push_all(job.handle, bad, check=False) == phub.PHUB_EINVAL
+    assert "aligned" in lib.last_error()
+    assert lib.phub_step(job.handle, check=False) == phub.PHUB_ENOTREADY
+    assert lib.phub_push_all(job.handle, None, check=False) == phub.PHUB_EINVAL
+    lib.phub_push_all(job.handle, table)
+    lib.phub_step(job.handle)
+    job.sync()
     job.destroy()
 
 
