@@ -388,6 +388,10 @@ def main(argv=None) -> int:
     ap.add_argument("--producer-mb", type=float, default=8.0,
                     help="--streaming: the simulated backward writes its gradients in buckets "
                          "of this many MB per worker, one event each")
+    ap.add_argument("--workgroups", type=int, default=None,
+                    help="ablation: workgroups of each launch (default one per compute unit, "
+                         "persistent); a value of at least a quarter of the job's tiles gives "
+                         "every wave at most one item, the non-persistent form")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="after the timed steps, this many more with the memory-side cache "
                          "flushed before each job's step (a 1 GiB read); reported as "
@@ -441,7 +445,8 @@ def main(argv=None) -> int:
         job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
                        chunk_bytes=args.chunk_bytes, unfused=args.unfused,
                        optimizer=None if args.optimizer == "momentum" else args.optimizer,
-                       schedule=None if args.schedule == "lpt" else PHUB_SCHEDULE_SPLIT)
+                       schedule=None if args.schedule == "lpt" else PHUB_SCHEDULE_SPLIT,
+                       workgroups=args.workgroups)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
              for w in range(spec.num_workers)]
@@ -549,6 +554,7 @@ def main(argv=None) -> int:
                      for j, r in zip(wl.jobs, cached)],
             "chunk_bytes": args.chunk_bytes or wl.jobs[0].chunk_bytes,
             "schedule": args.schedule,
+            "workgroups_option": args.workgroups,
             "optimizer": ({"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
                            "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov}
                           if args.optimizer == "momentum" else
