@@ -470,15 +470,20 @@ def _sample_positions(spec, rng, n_random=20000):
     return sorted(pos)
 
 
-@pytest.mark.parametrize("name", ["resnet50", "alexnet", "resnet269", "multitenant"])
-def test_full_size_workload_sampled(lib, torch_dev, name):
+@pytest.mark.parametrize("name,own_streams", [("resnet50", False), ("alexnet", False),
+                                               ("resnet269", False), ("multitenant", False),
+                                               ("multitenant", True)])
+def test_full_size_workload_sampled(lib, torch_dev, name, own_streams):
+    """As the benchmark runs it: the jobs of a multi-job workload share one
+    stream (and, as the ablation, each has its own)."""
     torch, dev = torch_dev
     wl = workloads.workload(name)
     steps = 2
-    _say("full size", name, workloads.describe(wl))
+    _say("full size", name, "own streams" if own_streams else "", workloads.describe(wl))
+    shared = torch.cuda.Stream(device=dev)
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
-        stream = torch.cuda.Stream(device=dev)
+        stream = torch.cuda.Stream(device=dev) if own_streams else shared
         job = TorchJob(spec, dev, stream=stream, lib=lib)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         job.set_weights(w0)
