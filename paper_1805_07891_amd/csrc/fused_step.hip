@@ -274,25 +274,34 @@ __device__ __forceinline__ void tile_streams(TileStreams<NW, S>& s, const DevTil
 // Issue order of a tile's loads: for each of the kVecPerLane pieces, the S
 // state arrays (W first), then the gradients in worker order; kTileLoads
 // loads per tile.  A wave keeps a window of loads in flight beyond the one
-// it waits for, and the window runs on into the wave's next tile.  Its
-// depth follows the state policy (measured on MI355X):
-//  - non-temporal state: a shallow window (kShallowAhead loads, a few KB
-//    per wave) with the state reads and writes spread through the tile
-//    moves more bytes than a deep one; deep windows flood the memory system
-//    with open streams;
+// it waits for, and the window runs on into the wave's next tile.  The ring
+// of loads in flight must divide the tile's loads, so that every load keeps
+// its register slot from one tile to the next.  Its depth follows the state
+// policy (measured on MI355X):
+//  - non-temporal state: a shallow window, with the state reads and writes
+//    spread through the tile.  Loads and stores share one in-order counter,
+//    so a load issued after a state store is consumed only once that store
+//    has completed, and the depth sets the time a store gets.  Five loads
+//    ahead (a ring of 6) is 1-2 points better than three, for every worker
+//    count it divides the tile of; deeper windows (7 to 35 ahead) are no
+//    better or worse, as they flood the memory system with open streams.
+//    Where a ring of 6 does not divide the tile, three ahead;
 //  - state held in the memory-side cache: a whole tile ahead (every load of
 //    the next tile in flight while this one is consumed), since only the
 //    gradient streams then reach HBM.
-#ifndef PHUB_LOADS_AHEAD
-#define PHUB_LOADS_AHEAD 3
-#endif
-constexpr int kShallowAhead = PHUB_LOADS_AHEAD;
-
 template <int NW, int S>
 constexpr int kTileLoads = kVecPerLane * (NW + S);
 
+#ifdef PHUB_LOADS_AHEAD
+template <int NW, int S>
+constexpr int kShallowAhead = PHUB_LOADS_AHEAD;  // a fixed depth, for sweeps
+#else
+template <int NW, int S>
+constexpr int kShallowAhead = kTileLoads<NW, S> % 6 == 0 ? 5 : 3;
+#endif
+
 template <int NW, int S, bool RES>
-constexpr int kAhead = RES ? kTileLoads<NW, S> - 1 : kShallowAhead;
+constexpr int kAhead = RES ? kTileLoads<NW, S> - 1 : kShallowAhead<NW, S>;
 
 template <int NW, int S, bool RES>
 constexpr int kRing = kAhead<NW, S, RES> + 1;
