@@ -227,10 +227,12 @@ def streaming_bench(torch, dev, lib, wl, args) -> int:
     per bucket; the host pushes each bucket's keys with that event at once.
     Each bucket is first computed on the same GPU (bf16 GEMMs proportional
     to the bucket's parameters: the layers' backward work), then written.
-    Timed on the device from the start of the backward to the end of the
-    step, for one launch at phub_step and for readiness groups of
-    --bucket-mb launched as they complete; the backward alone is the
-    baseline, and the exposed time is what the step adds after it."""
+    With --arrival link, the buckets instead arrive through one ingress
+    stream at N times --link-gbps (a sleep kernel paces them, then they are
+    copied into place as a network card's DMA would).  For one launch at
+    phub_step and for readiness groups of --bucket-mb launched as they
+    complete, the exposed time is measured within each run on the device:
+    the end of the step minus the end of the last producer's work.""" 
     import statistics
     from paper_1805_07891_amd import workloads
     from paper_1805_07891_amd.job import TorchJob
@@ -245,12 +247,39 @@ def streaming_bench(torch, dev, lib, wl, args) -> int:
                              / spec.num_params / flop_per_mm))) for b in buckets]
     weight = torch.randn(dim, dim, device=dev, dtype=torch.bfloat16)
     acts = [torch.randn(mrows, dim, device=dev, dtype=torch.bfloat16) for _ in range(N)]
+    link = args.arrival == "link"
+    # link arrival: one ingress stream.  Streams share the process's few
+    # hardware queues in creation order, so the run creates no stream it does
+    # not use (a job's stream sharing a queue with the ingress would run its
+    # launches in line with the arrivals).
+    producers = [torch.cuda.Stream(device=dev) for _ in range(1 if link else N)]
+    sleep_cycles = []
+    if link:
+        # calibrate the sleep kernel: cycles per microsecond of device time
+        cal = producers[0]
+        rates = []
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(cal):
+                e0.record(cal)
+                torch.cuda._sleep(1 << 22)
+                e1.record(cal)
+            torch.cuda.synchronize()
+            rates.append((1 << 22) / (e0.elapsed_time(e1) * 1e3))
+        per_us = statistics.median(rates)
+        # one ingress for all workers (the server's network), N links' worth of rate:
+        # a bucket of every worker arrives in its bytes / (N * link rate)
+        link_bytes_per_us = args.link_gbps * 1e9 / 8 / 1e6
+        sleep_cycles = [max(1, int(4 * sum(spec.key_elems[k] for k in b) / link_bytes_per_us * per_us))
+                        for b in buckets]
     src = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, 0, 0, w) for w in range(N)]
     w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, 0)
-    producers = [torch.cuda.Stream(device=dev) for _ in range(N)]
+
     jobs = {}
     for mode, kg in (("one_launch", None), ("groups", key_group)):
-        job = TorchJob(spec, dev, lib=lib, key_group=kg)
+        # each worker's bucket events are recorded on its own producer stream,
+        # in push order
+        job = TorchJob(spec, dev, lib=lib, key_group=kg, ordered_events=not args.unordered_events)
         job.set_weights(w0)
         arenas = [torch.zeros_like(src[w]) for w in range(N)]
         for w in range(N):
@@ -268,57 +297,89 @@ def streaming_bench(torch, dev, lib, wl, args) -> int:
     def backward(job, arenas, pushes):
         start = torch.cuda.Event(enable_timing=True)
         start.record(producers[0])
-        for w in range(1, N):
-            producers[w].wait_event(start)
+        for p in producers[1:]:
+            p.wait_event(start)
         events = []
+        arrived = []   # per producer stream: timed marker after its last bucket
+        last = len(buckets) - 1
         for bi in range(len(buckets)):
             lo, hi = bounds[bi]
+            if link:
+                # the ingress stream delivers bucket bi of every worker, then one event
+                with torch.cuda.stream(producers[0]):
+                    torch.cuda._sleep(sleep_cycles[bi])
+                    for w in range(N):
+                        arenas[w][lo:hi].copy_(src[w][lo:hi])
+                    ev = torch.cuda.Event(enable_timing=bi == last)
+                    ev.record(producers[0])
+                events.append(ev)
+                if bi == last:
+                    arrived.append(ev)
+                if pushes is not None:
+                    for w in range(N):
+                        job.push_bucket(w, pushes[w][bi], ev)
+                continue
             for w in range(N):
                 with torch.cuda.stream(producers[w]):
                     for _ in range(n_mm[bi]):
                         torch.mm(acts[w], weight)
                     arenas[w][lo:hi].copy_(src[w][lo:hi])
-                    ev = torch.cuda.Event()
+                    ev = torch.cuda.Event(enable_timing=bi == last)
                     ev.record(producers[w])
                 events.append(ev)
+                if bi == last:
+                    arrived.append(ev)
                 if pushes is not None:
                     job.push_bucket(w, pushes[w][bi], ev)
-        return start, events
+        return start, arrived
 
     def run(mode, reps):
+        """(start to end, last arrival to end) in us for each repetition."""
         out = []
         for _ in range(reps):
             job, arenas, pushes = jobs["one_launch"] if mode == "backward_only" else jobs[mode]
-            start, events = backward(job, arenas, None if mode == "backward_only" else pushes)
+            # arrived: the end of every producer stream's work, recorded before
+            # the push that may enqueue the last group
+            start, arrived = backward(job, arenas, None if mode == "backward_only" else pushes)
             end = torch.cuda.Event(enable_timing=True)
             if mode == "backward_only":
-                for w in range(1, N):
-                    producers[0].wait_stream(producers[w])
+                for p in producers[1:]:
+                    producers[0].wait_stream(p)
                 end.record(producers[0])
             else:
                 job.step()
                 end.record(job.stream)
             torch.cuda.synchronize()
-            out.append(start.elapsed_time(end) * 1e3)
+            out.append((start.elapsed_time(end) * 1e3,
+                        min(e.elapsed_time(end) for e in arrived) * 1e3))
         return out
 
-    print(f"streaming: {wl.name}, {N} workers, {len(buckets)} buckets per worker "
-          f"({sum(n_mm)} GEMMs of {mrows}x{dim}x{dim}), {ngroups} readiness groups",
-          file=sys.stderr, flush=True)
+    print(f"streaming: {wl.name}, {N} workers, {len(buckets)} buckets per worker, "
+          + (f"arriving at {args.link_gbps} Gb/s per worker" if link else
+             f"{sum(n_mm)} GEMMs of {mrows}x{dim}x{dim}")
+          + f", {ngroups} readiness groups", file=sys.stderr, flush=True)
     for mode in ("backward_only", "one_launch", "groups"):
         print(f"streaming: warm-up {mode}", file=sys.stderr, flush=True)
         run(mode, 3)
     reps = max(5, args.steps // 25)
     t = {m: [] for m in ("backward_only", "one_launch", "groups")}
+    after = {m: [] for m in ("one_launch", "groups")}
     for r in range(reps):                       # interleaved, so drift hits every mode
         for m in t:
-            t[m] += run(m, 1)
-        print(f"streaming: rep {r + 1}/{reps}: " + ", ".join(f"{m} {v[-1]:.0f} us" for m, v in t.items()),
+            total, tail = run(m, 1)[0]
+            t[m].append(total)
+            if m in after:
+                after[m].append(tail)
+        print(f"streaming: rep {r + 1}/{reps}: " + ", ".join(f"{m} {v[-1]:.0f} us" for m, v in t.items())
+              + "; after the last arrival: " + ", ".join(f"{m} {v[-1]:.0f} us" for m, v in after.items()),
               file=sys.stderr, flush=True)
     med = {m: statistics.median(v) for m, v in t.items()}
+    med_after = {m: statistics.median(v) for m, v in after.items()}
     out = {
-        "metric": "exchange time exposed after the backward pass (step end - backward end)",
-        "value": round(med["groups"] - med["backward_only"], 1),
+        "metric": ("exchange time exposed after the last gradient arrives (step end - arrival end)"
+                   if link else
+                   "exchange time exposed after the backward pass (step end - backward end)"),
+        "value": round(med_after["groups"], 1),
         "unit": "us",
         "higher_is_better": False,
         "n_gpus": 1,
@@ -328,14 +389,21 @@ def streaming_bench(torch, dev, lib, wl, args) -> int:
         "config": {"workload": wl.name, "job": spec.name, "workers": N, "keys": K,
                    "params": spec.num_params, "readiness_groups": ngroups,
                    "bucket_mb": args.bucket_mb, "producer_buckets": nprod,
-                   "producer_mb": args.producer_mb, "gemm": [mrows, dim, dim],
-                   "bf16_tflop_per_worker": args.backward_tflop},
+                   "producer_mb": args.producer_mb,
+                   "ordered_events": not args.unordered_events,
+                   **({"arrival": "link", "link_gbps_per_worker": args.link_gbps}
+                      if link else
+                      {"arrival": "gemm", "gemm": [mrows, dim, dim],
+                       "bf16_tflop_per_worker": args.backward_tflop})},
         "median_us": {m: round(v, 1)
                       for m, v in med.items()},
         "min_us": {m: round(min(v), 1)
                    for m, v in t.items()},
-        "exposed_us": {"one_launch": round(med["one_launch"] - med["backward_only"], 1),
-                       "groups": round(med["groups"] - med["backward_only"], 1)},
+        # measured within each run: step end - end of the last producer's work
+        "exposed_us": {m: round(v, 1) for m, v in med_after.items()},
+        # difference of medians over separate runs (noisier: producer time varies)
+        "total_minus_producers_only_us": {m: round(med[m] - med["backward_only"], 1)
+                                          for m in ("one_launch", "groups")},
     }
     print(json.dumps(out), flush=True)
     for job, _, _ in jobs.values():
@@ -383,6 +451,18 @@ def main(argv=None) -> int:
                          "simulated backward pass, one launch vs readiness groups")
     ap.add_argument("--bucket-mb", type=float, default=25.0,
                     help="readiness group size for --streaming (MB of fp32 gradient per worker)")
+    ap.add_argument("--arrival", choices=("gemm", "link"), default="gemm",
+                    help="--streaming: how gradients become ready: computed by a simulated "
+                         "backward on the same GPU (gemm), or arriving at a fixed link rate per "
+                         "worker, paced by a sleep kernel then copied into place as a network "
+                         "card's DMA would (link)")
+    ap.add_argument("--link-gbps", type=float, default=56.0,
+                    help="--streaming --arrival link: per-worker link rate in Gb/s (the paper's "
+                         "InfiniBand interfaces run at 56); all workers' buckets arrive through "
+                         "one ingress stream at N times that rate")
+    ap.add_argument("--unordered-events", action="store_true",
+                    help="--streaming: do not tell the library that each worker's events are "
+                         "ordered on its stream (every distinct event is then waited for)")
     ap.add_argument("--backward-tflop", type=float, default=1.0,
                     help="--streaming: simulated backward work per worker (bf16 TFLOP)")
     ap.add_argument("--producer-mb", type=float, default=8.0,
@@ -404,6 +484,12 @@ def main(argv=None) -> int:
                     help="first run a plain 512 MiB device copy three times (a known-size "
                          "reference for hardware byte counters)")
     args = ap.parse_args(argv)
+
+    if args.streaming and "GPU_MAX_HW_QUEUES" not in os.environ:
+        # one hardware queue per stream (set before the HIP runtime starts):
+        # producer streams that shared a queue with the job's stream would run
+        # its launches in line with their own work
+        os.environ["GPU_MAX_HW_QUEUES"] = "16"
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the exchange step here runs on a single "

@@ -155,6 +155,17 @@ typedef struct phub_options {
                                element instead of (N + 4) * 4).  Same
                                results.  Not with readiness groups or
                                pushpull (PHUB_EINVAL).  0: fused (default). */
+    int ordered_events;     /* 1: the caller guarantees that each worker's
+                               ready events (phub_push_event and the batched
+                               forms) are recorded on one stream, in the
+                               order of its pushes; a launch then waits only
+                               for each worker's last event among the keys it
+                               covers (at most num_workers waits instead of
+                               one per distinct event; each wait costs device
+                               time when it resolves).  0 (default): every
+                               distinct event is waited for.  Either way,
+                               events already complete when the launch is
+                               enqueued are not waited for. */
 } phub_options;
 
 /*

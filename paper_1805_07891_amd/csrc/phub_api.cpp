@@ -146,6 +146,8 @@ struct phub_job {
 
     std::vector<const float*> grads;  // host table, [row * N + worker]
     std::vector<hipEvent_t> ready;    // same layout: event to wait for (none if null)
+    bool ordered_events = false;      // each worker's events are ordered on one stream
+    std::vector<hipEvent_t> group_last_event;  // [group * N + worker]: last event pushed this step
     std::vector<uint8_t> pushed;      // same layout: pushed since the last step
     int64_t num_pushed = 0;
     std::vector<float*> outs;         // same layout: pushpull model buffers of this step
@@ -326,14 +328,25 @@ int launch_group(phub_job* j, int g) {
         if (int rc = upload_rows(j, g)) return rc;
     if (pull && j->rgroup_out_dirty[g])
         if (int rc = upload_out_rows(j, g)) return rc;
+    // The events to wait for: every distinct one of the group's pushes, or
+    // with ordered events each worker's last one; events already complete
+    // need no wait.
     std::vector<hipEvent_t> evs;
-    for (size_t i = size_t(j->rgroup_row_begin[g]) * n; i < size_t(j->rgroup_row_begin[g + 1]) * n;
-         ++i)
-        if (j->ready[i]) evs.push_back(j->ready[i]);
+    if (j->ordered_events) {
+        for (size_t w = 0; w < n; ++w)
+            if (hipEvent_t ev = j->group_last_event[size_t(g) * n + w]) evs.push_back(ev);
+    } else {
+        for (size_t i = size_t(j->rgroup_row_begin[g]) * n;
+             i < size_t(j->rgroup_row_begin[g + 1]) * n; ++i)
+            if (j->ready[i]) evs.push_back(j->ready[i]);
+    }
     std::sort(evs.begin(), evs.end());
     evs.erase(std::unique(evs.begin(), evs.end()), evs.end());
     for (hipEvent_t ev : evs) {
-        hipError_t e = hipStreamWaitEvent(j->stream, ev, 0);
+        hipError_t e = hipEventQuery(ev);
+        if (e == hipSuccess) continue;
+        if (e != hipErrorNotReady) return hip_fail(e, "hipEventQuery (ready event)");
+        e = hipStreamWaitEvent(j->stream, ev, 0);
         if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent (ready event)");
     }
     if (j->rgroup_work[g]) {
@@ -392,6 +405,7 @@ int record_push(phub_job* j, int worker, int key, const float* grad, hipEvent_t 
         j->rgroup_dirty[g] = 1;
     }
     j->ready[i] = ev;
+    if (ev && j->ordered_events) j->group_last_event[size_t(g) * j->num_workers + worker] = ev;
     if (!j->pushed[i]) {
         j->pushed[i] = 1;
         ++j->num_pushed;
@@ -477,6 +491,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     int optimizer = PHUB_OPT_MOMENTUM;
     float beta1 = 0, beta2 = 0, eps = 0;
     int workgroups = 0;  // 0: one per compute unit
+    bool ordered_events = false;
     if (options) {
         if (options->workgroups < 0 || options->workgroups > kMaxWorkgroups)
             return fail(PHUB_EINVAL, "workgroups must be in [0, %d], got %d", kMaxWorkgroups,
@@ -516,6 +531,9 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         if (options->resident_bytes >= 0) resident_bytes = options->resident_bytes;
         num_rgroups = options->num_groups;
         unfused = options->unfused != 0;
+        if (options->ordered_events != 0 && options->ordered_events != 1)
+            return fail(PHUB_EINVAL, "ordered_events must be 0 or 1, got %d", options->ordered_events);
+        ordered_events = options->ordered_events == 1;
     }
 
     phub_job* j = new (std::nothrow) phub_job;
@@ -544,6 +562,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->eps = eps;
         j->grads.assign(size_t(num_workers) * num_keys, nullptr);
         j->ready.assign(size_t(num_workers) * num_keys, nullptr);
+        j->ordered_events = ordered_events;
         j->pushed.assign(size_t(num_workers) * num_keys, 0);
         j->outs.assign(size_t(num_workers) * num_keys, nullptr);
         j->has_out.assign(size_t(num_workers) * num_keys, 0);
@@ -564,6 +583,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             j->key_of_row[row] = k;
         }
         j->rgroup_work.assign(j->num_rgroups, 0);
+        j->group_last_event.assign(size_t(j->num_rgroups) * num_workers, nullptr);
         j->rgroup_pushed.assign(j->num_rgroups, 0);
         j->rgroup_launched.assign(j->num_rgroups, 0);
         j->rgroup_dirty.assign(j->num_rgroups, 1);
@@ -924,6 +944,7 @@ int phub_step(phub_job* j) {
             if (int rc = launch_group(j, g)) return rc;
     std::fill(j->pushed.begin(), j->pushed.end(), 0);
     std::fill(j->ready.begin(), j->ready.end(), nullptr);
+    std::fill(j->group_last_event.begin(), j->group_last_event.end(), nullptr);
     std::fill(j->rgroup_pushed.begin(), j->rgroup_pushed.end(), 0);
     std::fill(j->rgroup_launched.begin(), j->rgroup_launched.end(), 0);
     std::fill(j->has_out.begin(), j->has_out.end(), 0);

@@ -58,7 +58,7 @@ class TorchJob:
                  resident_bytes: Optional[int] = None,
                  key_group: Optional[Sequence[int]] = None, unfused: bool = False,
                  optimizer: Optional[str] = None, betas=(0.9, 0.999), eps: float = 1e-8,
-                 workgroups: Optional[int] = None):
+                 workgroups: Optional[int] = None, ordered_events: bool = False):
         import torch
         self.torch = torch
         self.spec = spec
@@ -76,7 +76,8 @@ class TorchJob:
                                              optimizer=None if optimizer is None
                                              else _phub.OPTIMIZERS[optimizer],
                                              beta1=betas[0], beta2=betas[1], eps=eps,
-                                             workgroups=workgroups)
+                                             workgroups=workgroups,
+                                             ordered_events=int(bool(ordered_events)))
         self.optimizer = optimizer or "momentum"
         self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers

@@ -45,11 +45,11 @@ class Case:
     """A job with seeded weights, plus the oracle's copy of its state."""
 
     def __init__(self, torch, dev, lib, n_workers, key_elems, key_group=None, seed=0,
-                 resident_bytes=None):
+                 resident_bytes=None, ordered_events=False):
         self.torch, self.dev = torch, dev
         self.spec = Job("stream", n_workers, tuple(int(n) for n in key_elems), sigma_g=1e-2)
         self.job = TorchJob(self.spec, dev, lib=lib, key_group=key_group,
-                            resident_bytes=resident_bytes)
+                            resident_bytes=resident_bytes, ordered_events=ordered_events)
         self.offs, self.total = key_offsets(self.spec.key_elems)
         self.rng = np.random.default_rng(seed)
         w0 = np.zeros(self.total, np.float32)
@@ -107,17 +107,25 @@ def test_groups_launched_as_they_complete_match_the_oracle(lib, torch_dev, group
     c.job.destroy()
 
 
-@pytest.mark.parametrize("grouped,batched", [(False, False), (True, False), (True, True)])
-def test_ready_events_are_waited_on(lib, torch_dev, grouped, batched):
+@pytest.mark.parametrize("grouped,batched,ordered", [
+    (False, False, False), (True, False, False), (True, True, False),
+    (False, False, True), (True, False, True), (True, True, True), ("pairs", False, True)])
+def test_ready_events_are_waited_on(lib, torch_dev, grouped, batched, ordered):
     """Producers fill the gradient buffers on their own streams after a
     delay and record an event per key; the host pushes right away.  The step
-    must read the produced values, not the zeros the buffers held."""
+    must read the produced values, not the zeros the buffers held.  Each
+    worker's events are recorded on its own stream in push order, so the
+    ordered-events option (a launch waits only for each worker's last event
+    among its keys) holds too."""
     torch, dev = torch_dev
     keys = (300000, 70001, 8193, 1024, 5)
     n_workers = 4
-    key_group = list(range(len(keys))) if grouped else None
-    _say("ready events,", "grouped" if grouped else "one launch", "batched" if batched else "per key")
-    c = Case(torch, dev, lib, n_workers, keys, key_group=key_group, seed=12)
+    key_group = ([k // 2 for k in range(len(keys))] if grouped == "pairs" else
+                 list(range(len(keys))) if grouped else None)
+    _say("ready events,", "grouped" if grouped else "one launch", "batched" if batched else "per key",
+         "ordered" if ordered else "")
+    c = Case(torch, dev, lib, n_workers, keys, key_group=key_group, seed=12,
+             ordered_events=ordered)
     host = c.host_grads()
     src = [torch.from_numpy(a).to(dev) for a in host]
     arenas = [torch.zeros(c.total, device=dev) for _ in range(n_workers)]
