@@ -111,10 +111,18 @@ def test_optimizer_matches_the_oracle(lib, torch_dev, optimizer, n_workers, resi
 
 
 @pytest.mark.parametrize("optimizer", ["sgd", "adam"])
-def test_optimizer_with_groups_pushpull_and_unfused(lib, torch_dev, optimizer):
+@pytest.mark.parametrize("resident", [None, 12 * 30000])
+def test_optimizer_with_groups_pushpull_and_unfused(lib, torch_dev, optimizer, resident):
+    """Readiness groups + pushpull (every group of a step uses the same step
+    number), then the unfused ablation; with the default budget (all state
+    cached) and with a budget that ends inside a key (both bins in every
+    group's launch)."""
     torch, dev = torch_dev
-    # readiness groups + pushpull: every group of a step uses the same step number
-    c = Case(torch, dev, lib, optimizer, 8, KEYS, seed=61, key_group=[k % 3 for k in range(len(KEYS))])
+    _say(optimizer, "groups + pushpull, resident", resident)
+    c = Case(torch, dev, lib, optimizer, 8, KEYS, seed=61, key_group=[k % 3 for k in range(len(KEYS))],
+             resident_bytes=resident)
+    frac = c.job.cached_fraction()
+    assert frac == 1.0 if resident is None else 0.0 < frac < 1.0
     models = [torch.full((c.total,), float("nan"), device=dev) for _ in range(8)]
     for w in range(8):
         c.job.attach_models(w, models[w])
@@ -130,7 +138,7 @@ def test_optimizer_with_groups_pushpull_and_unfused(lib, torch_dev, optimizer):
                 assert _bits_equal(mh[o:o + n], c.W[k]), f"model buffer {w} key {k}"
     c.job.destroy()
     # the unfused ablation with the same optimizer
-    c = Case(torch, dev, lib, optimizer, 5, KEYS, seed=62, unfused=True)
+    c = Case(torch, dev, lib, optimizer, 5, KEYS, seed=62, unfused=True, resident_bytes=resident)
     for t in range(2):
         host, _ = c.new_grads()
         c.job.push_all()

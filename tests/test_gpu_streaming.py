@@ -107,10 +107,11 @@ def test_groups_launched_as_they_complete_match_the_oracle(lib, torch_dev, group
     c.job.destroy()
 
 
-@pytest.mark.parametrize("grouped,batched,ordered", [
-    (False, False, False), (True, False, False), (True, True, False),
-    (False, False, True), (True, False, True), (True, True, True), ("pairs", False, True)])
-def test_ready_events_are_waited_on(lib, torch_dev, grouped, batched, ordered):
+@pytest.mark.parametrize("grouped,batched,ordered,resident", [
+    (False, False, False, None), (True, False, False, None), (True, True, False, None),
+    (False, False, True, None), (True, False, True, None), (True, True, True, None),
+    ("pairs", False, True, None), ("pairs", True, True, 8 * 100000), (False, False, True, 0)])
+def test_ready_events_are_waited_on(lib, torch_dev, grouped, batched, ordered, resident):
     """Producers fill the gradient buffers on their own streams after a
     delay and record an event per key; the host pushes right away.  The step
     must read the produced values, not the zeros the buffers held.  Each
@@ -125,7 +126,7 @@ def test_ready_events_are_waited_on(lib, torch_dev, grouped, batched, ordered):
     _say("ready events,", "grouped" if grouped else "one launch", "batched" if batched else "per key",
          "ordered" if ordered else "")
     c = Case(torch, dev, lib, n_workers, keys, key_group=key_group, seed=12,
-             ordered_events=ordered)
+             ordered_events=ordered, resident_bytes=resident)
     host = c.host_grads()
     src = [torch.from_numpy(a).to(dev) for a in host]
     arenas = [torch.zeros(c.total, device=dev) for _ in range(n_workers)]
