@@ -476,10 +476,10 @@ def main(argv=None) -> int:
                     help="after the timed steps, this many more with the memory-side cache "
                          "flushed before each job's step (a 1 GiB read); reported as "
                          "roofline.cold (0 skips)")
-    ap.add_argument("--own-streams", action="store_true",
-                    help="multi-job workloads: each job on its own stream, its launches "
-                         "running concurrently with the other jobs' (default: the jobs "
-                         "share one stream and take turns, each launch with the whole GPU)")
+    ap.add_argument("--shared-stream", action="store_true",
+                    help="multi-job workloads: the jobs share one stream and take turns, each "
+                         "launch with the whole GPU (default: each job on its own stream, its "
+                         "launches concurrent with the other jobs')")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 512 MiB device copy three times (a known-size "
                          "reference for hardware byte counters)")
@@ -520,10 +520,10 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    # Co-running jobs share one stream by default: their steps take turns,
-    # each launch with the whole GPU (measured faster than concurrent launches
-    # on separate streams, which compete for HBM and stretch each other).
-    shared_stream = len(wl.jobs) > 1 and not args.own_streams
+    # Co-running jobs each have their own stream (their launches run
+    # concurrently); with --shared-stream they take turns on one stream,
+    # each launch with the whole GPU.
+    shared_stream = len(wl.jobs) > 1 and args.shared_stream
     one_stream = torch.cuda.Stream(device=dev)
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
@@ -606,18 +606,29 @@ def main(argv=None) -> int:
     durs = sorted(ev[dom][s][0].elapsed_time(ev[dom][s][1]) for s in range(K))
     per_launch_avg_ms = sum(durs) / len(durs)
     med_ms = durs[len(durs) // 2]
-    # Its average launch duration: K launches of that job back to back on its
-    # stream between one pair of HIP events (an event pair around every
-    # launch adds 2-5 us to each; the spread above comes from those).
-    djob = jobs[dom]
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(djob.stream)
-    for _ in range(K):
-        push(djob)
-        djob.step()
-    e1.record(djob.stream)
-    torch.cuda.synchronize()
-    avg_ms = e0.elapsed_time(e1) / K
+    # Its average launch duration.  Where the dominant job's kernels run one
+    # after another with nothing else on its stream (one job, or jobs taking
+    # turns on a shared stream): K launches of that job back to back between
+    # one pair of HIP events (an event pair around every launch adds 2-5 us
+    # to each; the spread above comes from those).  With a stream per job the
+    # jobs' launches run concurrently and their streams share the process's
+    # hardware queues, so the stream's time is not the kernel's: the mean of
+    # the per-launch events is taken.
+    if len(jobs) == 1 or shared_stream:
+        djob = jobs[dom]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(djob.stream)
+        for _ in range(K):
+            push(djob)
+            djob.step()
+        e1.record(djob.stream)
+        torch.cuda.synchronize()
+        avg_ms = e0.elapsed_time(e1) / K
+        avg_kind = "K launches back to back on the job's stream between one pair of HIP events"
+    else:
+        avg_ms = per_launch_avg_ms
+        avg_kind = ("mean of HIP event pairs around each launch, the jobs' launches "
+                    "concurrent on their own streams")
     dom_bytes = job_bytes(wl.jobs[dom])
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
     traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum")
@@ -680,7 +691,7 @@ def main(argv=None) -> int:
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "avg_launch_us": round(avg_ms * 1e3, 2),
-            "avg_launch_us_kind": "K launches back to back between one pair of HIP events",
+            "avg_launch_us_kind": avg_kind,
             "per_launch_events_us": {"avg": round(per_launch_avg_ms * 1e3, 2),
                                      "median": round(med_ms * 1e3, 2),
                                      "min": round(durs[0] * 1e3, 2)},

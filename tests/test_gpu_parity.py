@@ -470,12 +470,12 @@ def _sample_positions(spec, rng, n_random=20000):
     return sorted(pos)
 
 
-@pytest.mark.parametrize("name,own_streams", [("resnet50", False), ("alexnet", False),
-                                               ("resnet269", False), ("multitenant", False),
-                                               ("multitenant", True)])
+@pytest.mark.parametrize("name,own_streams", [("resnet50", True), ("alexnet", True),
+                                               ("resnet269", True), ("multitenant", True),
+                                               ("multitenant", False)])
 def test_full_size_workload_sampled(lib, torch_dev, name, own_streams):
-    """As the benchmark runs it: the jobs of a multi-job workload share one
-    stream (and, as the ablation, each has its own)."""
+    """As the benchmark runs it: the jobs of a multi-job workload each on
+    their own stream (and, as the option, all on one shared stream)."""
     torch, dev = torch_dev
     wl = workloads.workload(name)
     steps = 2
