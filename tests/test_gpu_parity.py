@@ -521,3 +521,32 @@ def test_full_size_workload_sampled(lib, torch_dev, name, own_streams):
         job.destroy()
     del grads
     torch.cuda.empty_cache()
+
+
+def test_jobs_driven_from_several_threads(lib, torch_dev):
+    """Different jobs may be driven from different threads: each thread
+    creates its own job (claiming from the shared cache budget), steps it
+    and checks it against the oracle, then destroys it; the threads run at
+    the same time, several rounds."""
+    import threading
+    torch, dev = torch_dev
+    errors = []
+
+    def work(i):
+        try:
+            torch.cuda.set_device(dev)
+            for r in range(3):
+                keys = [1000 + 37 * i, 70001, 5 + r]
+                job, res = run_small_case(torch, dev, lib, 3 + i, keys, steps=2, seed=500 + 10 * i + r,
+                                          stream=torch.cuda.Stream(device=dev))
+                assert_parity(res, f"thread {i} round {r}")
+                job.destroy()
+        except Exception as e:  # reported by the main thread
+            errors.append(f"thread {i}: {e!r}")
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
