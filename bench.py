@@ -121,6 +121,34 @@ def read_ceiling(torch, dev, arenas, reps: int = 5):
             "bytes": len(arenas) * n * 4}
 
 
+def cu_masked_streams(torch, dev, wl):
+    """(stream, compute units) per job: HIP streams restricted to disjoint
+    sets of compute units, in proportion to each job's bytes per step (at
+    least one each), wrapped as torch external streams."""
+    import ctypes
+    from paper_1805_07891_amd.job import hip_runtime
+    hip = hip_runtime()
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    by = [j.hbm_bytes_per_step() for j in wl.jobs]
+    share = [max(1, int(cus * b / sum(by))) for b in by]
+    share[by.index(max(by))] += cus - sum(share)     # the rest to the largest job
+    hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
+                                                 ctypes.POINTER(ctypes.c_uint32)]
+    hip.hipExtStreamCreateWithCUMask.restype = ctypes.c_int
+    out, first = [], 0
+    for n in share:
+        words = (ctypes.c_uint32 * ((cus + 31) // 32))()
+        for cu in range(first, first + n):
+            words[cu // 32] |= 1 << (cu % 32)
+        first += n
+        handle = ctypes.c_void_p()
+        rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(handle), len(words), words)
+        if rc != 0:
+            raise RuntimeError(f"hipExtStreamCreateWithCUMask failed: {rc}")
+        out.append((torch.cuda.ExternalStream(handle.value, device=dev), n))
+    return out
+
+
 def cold_launches(torch, dev, jobs, dom, push, steps: int, dom_bytes: int):
     """The dominant job's kernel with a cold memory-side cache: before each
     job's step, a 1 GiB buffer is read with ordinary (cache-allocating)
@@ -476,6 +504,10 @@ def main(argv=None) -> int:
                     help="after the timed steps, this many more with the memory-side cache "
                          "flushed before each job's step (a 1 GiB read); reported as "
                          "roofline.cold (0 skips)")
+    ap.add_argument("--cu-masks", action="store_true",
+                    help="ablation for multi-job workloads: each job on its own stream restricted "
+                         "to a disjoint set of compute units in proportion to its bytes, with a "
+                         "persistent grid of that many workgroups")
     ap.add_argument("--shared-stream", action="store_true",
                     help="multi-job workloads: the jobs share one stream and take turns, each "
                          "launch with the whole GPU (default: each job on its own stream, its "
@@ -525,14 +557,17 @@ def main(argv=None) -> int:
     # each launch with the whole GPU.
     shared_stream = len(wl.jobs) > 1 and args.shared_stream
     one_stream = torch.cuda.Stream(device=dev)
+    masked = cu_masked_streams(torch, dev, wl) if args.cu_masks and len(wl.jobs) > 1 else None
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
         stream = one_stream if shared_stream or ji == 0 else torch.cuda.Stream(device=dev)
+        if masked is not None:
+            stream = masked[ji][0]
         job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
                        chunk_bytes=args.chunk_bytes, unfused=args.unfused,
                        optimizer=None if args.optimizer == "momentum" else args.optimizer,
                        schedule=None if args.schedule == "lpt" else PHUB_SCHEDULE_SPLIT,
-                       workgroups=args.workgroups)
+                       workgroups=masked[ji][1] if masked is not None else args.workgroups)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
              for w in range(spec.num_workers)]
@@ -675,7 +710,9 @@ def main(argv=None) -> int:
             "optimizer_kind": args.optimizer,
             "unfused": args.unfused,
             "streams": ("one shared by the jobs" if shared_stream else
+                        "one per job, CU-masked" if masked is not None else
                         "one per job" if len(wl.jobs) > 1 else "one"),
+            **({"cu_per_job": [m[1] for m in masked]} if masked is not None else {}),
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},
             "host_us_per_step": round(host_s * 1e6 / K, 2),
