@@ -665,6 +665,12 @@ def main(argv=None) -> int:
         avg_kind = ("mean of HIP event pairs around each launch, the jobs' launches "
                     "concurrent on their own streams")
     dom_bytes = job_bytes(wl.jobs[dom])
+    # every job's kernel (mean of its per-launch events)
+    per_job = []
+    for j, spec in enumerate(wl.jobs):
+        jm = sum(ev[j][s][0].elapsed_time(ev[j][s][1]) for s in range(K)) / K
+        per_job.append({"job": spec.name, "avg_launch_us": round(jm * 1e3, 2),
+                        "frac": round(job_bytes(spec) / (jm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
     traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum")
                else measured_traffic(args.workload))
@@ -732,6 +738,7 @@ def main(argv=None) -> int:
             "per_launch_events_us": {"avg": round(per_launch_avg_ms * 1e3, 2),
                                      "median": round(med_ms * 1e3, 2),
                                      "min": round(durs[0] * 1e3, 2)},
+            **({"per_job_events": per_job} if len(jobs) > 1 else {}),
             "measured_read_ceiling": ceiling,
             "frac_of_read_ceiling": round(achieved / ceiling["GBps"], 4),
             "cold": cold,
