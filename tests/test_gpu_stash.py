@@ -1,0 +1,103 @@
+"""GPU parity of the streamed bin's burst write-back (the LDS stash of the
+fixed-N kernels): every worker count and optimizer that has it, with
+grids small enough that a wave walks many tiles (several full write-backs
+and a partial last one), with nothing cached and with a cache budget that
+ends inside a key; bit-exact against the CPU oracle over two steps."""
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1805_07891_amd.job import TorchJob, load_library
+from paper_1805_07891_amd.workloads import Job, key_offsets
+
+pytestmark = pytest.mark.gpu
+
+LR, MU, WD, B1, B2, EPS = 0.05, 0.9, 1e-3, 0.9, 0.999, 1e-8
+
+# (workers, optimizer) of the kernels that stash: momentum and Nesterov with
+# 13 and 16 workers, plain SGD with 8, 11 and 14; and, next to them, counts
+# just below the rule (10 momentum, 5 SGD, 15 Adam) that write piece by piece
+STASHED = [(13, "momentum"), (13, "nesterov"), (16, "nesterov"), (16, "momentum"),
+           (8, "sgd"), (11, "sgd"), (14, "sgd"), (10, "momentum"), (5, "sgd"), (15, "adam")]
+# 107 full tiles and ragged ends: a wave of a 1-workgroup grid (4 waves)
+# walks about 27 tiles
+KEYS = (5, 1024 * 37 + 3, 70001, 1024 * 11, 4097, 1, 1024 * 6)
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    return torch, torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def lib(torch_dev):
+    return load_library()
+
+
+def _bits_equal(a, b):
+    return np.array_equal(np.asarray(a, np.float32).view(np.uint32),
+                          np.asarray(b, np.float32).view(np.uint32))
+
+
+@pytest.mark.parametrize("n,opt", STASHED)
+@pytest.mark.parametrize("workgroups,resident", [(1, 0), (3, 0), (1, "partial"), (None, 0),
+                                                 (None, "partial")])
+def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups, resident):
+    torch, dev = torch_dev
+    states = {"sgd": 1, "adam": 3}.get(opt, 2)
+    if resident == "partial":
+        resident = 4 * states * 50000
+    _say("stash", opt, "N", n, "workgroups", workgroups, "resident", resident)
+    spec = Job("stash", n, KEYS, lr=LR, momentum=MU, weight_decay=WD, nesterov=opt == "nesterov")
+    job = TorchJob(spec, dev, lib=lib, resident_bytes=resident, workgroups=workgroups,
+                   optimizer={"momentum": None, "nesterov": None}.get(opt, opt), betas=(B1, B2),
+                   eps=EPS)
+    offs, total = key_offsets(KEYS)
+    rng = np.random.default_rng(1000 + n)
+    w0 = np.zeros(total, np.float32)
+    for o, m in zip(offs, KEYS):
+        w0[o:o + m] = rng.standard_normal(m, dtype=np.float32) * np.float32(0.05)
+    job.set_weights(torch.from_numpy(w0).to(dev))
+    W = [w0[o:o + m].copy() for o, m in zip(offs, KEYS)]
+    M = [np.zeros(m, np.float32) for m in KEYS]
+    V = [np.zeros(m, np.float32) for m in KEYS]
+    for t in range(2):
+        host = []
+        for _ in range(n):
+            a = np.zeros(total, np.float32)
+            for o, m in zip(offs, KEYS):
+                a[o:o + m] = rng.standard_normal(m, dtype=np.float32) * np.float32(1e-2)
+            host.append(a)
+        arenas = [torch.from_numpy(a).to(dev) for a in host]
+        for w in range(n):
+            job.attach_grads(w, arenas[w])
+        torch.cuda.synchronize()
+        job.push_all()
+        job.step()
+        g = [[h[o:o + m] for o, m in zip(offs, KEYS)] for h in host]
+        if opt == "sgd":
+            oracle.step_sgd(g, W, LR, WD)
+        elif opt == "adam":
+            oracle.step_adam(g, W, M, V, LR, B1, B2, EPS, WD, t + 1)
+        else:
+            oracle.step(g, W, M, LR, MU, WD, opt == "nesterov")
+        Wg, Mg = job.state_arenas()
+        for k, (o, m) in enumerate(zip(offs, KEYS)):
+            assert _bits_equal(Wg[o:o + m], W[k]), f"step {t}: W key {k}"
+            if opt != "sgd":
+                assert _bits_equal(Mg[o:o + m], M[k]), f"step {t}: M key {k}"
+        if opt == "adam":
+            Vg = job.second_moment_arena()
+            for k, (o, m) in enumerate(zip(offs, KEYS)):
+                assert _bits_equal(Vg[o:o + m], V[k]), f"step {t}: V key {k}"
+    job.destroy()
