@@ -2,7 +2,8 @@
 fixed-N kernels): every worker count and optimizer that has it, with
 grids small enough that a wave walks many tiles (several full write-backs
 and a partial last one), with nothing cached and with a cache budget that
-ends inside a key; bit-exact against the CPU oracle over two steps."""
+ends inside a key, in one launch or one per readiness group; bit-exact
+against the CPU oracle over two steps."""
 
 import sys
 
@@ -49,19 +50,16 @@ def _bits_equal(a, b):
                           np.asarray(b, np.float32).view(np.uint32))
 
 
-@pytest.mark.parametrize("n,opt", STASHED)
-@pytest.mark.parametrize("workgroups,resident", [(1, 0), (3, 0), (1, "partial"), (None, 0),
-                                                 (None, "partial")])
-def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups, resident):
+def _run(lib, torch_dev, n, opt, workgroups, resident, key_group=None):
     torch, dev = torch_dev
     states = {"sgd": 1, "adam": 3}.get(opt, 2)
     if resident == "partial":
         resident = 4 * states * 50000
-    _say("stash", opt, "N", n, "workgroups", workgroups, "resident", resident)
+    _say("stash", opt, "N", n, "workgroups", workgroups, "resident", resident, "groups", key_group)
     spec = Job("stash", n, KEYS, lr=LR, momentum=MU, weight_decay=WD, nesterov=opt == "nesterov")
     job = TorchJob(spec, dev, lib=lib, resident_bytes=resident, workgroups=workgroups,
                    optimizer={"momentum": None, "nesterov": None}.get(opt, opt), betas=(B1, B2),
-                   eps=EPS)
+                   eps=EPS, key_group=key_group)
     offs, total = key_offsets(KEYS)
     rng = np.random.default_rng(1000 + n)
     w0 = np.zeros(total, np.float32)
@@ -82,7 +80,13 @@ def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups,
         for w in range(n):
             job.attach_grads(w, arenas[w])
         torch.cuda.synchronize()
-        job.push_all()
+        if key_group is None:
+            job.push_all()
+        else:
+            # backward order: each readiness group launches once its keys are in
+            for k in reversed(range(len(KEYS))):
+                for w in range(n):
+                    job.push_key(w, k)
         job.step()
         g = [[h[o:o + m] for o, m in zip(offs, KEYS)] for h in host]
         if opt == "sgd":
@@ -101,3 +105,19 @@ def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups,
             for k, (o, m) in enumerate(zip(offs, KEYS)):
                 assert _bits_equal(Vg[o:o + m], V[k]), f"step {t}: V key {k}"
     job.destroy()
+
+
+@pytest.mark.parametrize("n,opt", STASHED)
+@pytest.mark.parametrize("workgroups,resident", [(1, 0), (3, 0), (1, "partial"), (None, 0),
+                                                 (None, "partial")])
+def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups, resident):
+    _run(lib, torch_dev, n, opt, workgroups, resident)
+
+
+@pytest.mark.parametrize("n,opt", [(16, "nesterov"), (13, "momentum"), (11, "sgd")])
+@pytest.mark.parametrize("workgroups,resident", [(1, 0), (None, "partial")])
+def test_burst_write_back_per_readiness_group(lib, torch_dev, n, opt, workgroups, resident):
+    """Each readiness group's launch walks its own tiles: the stash is
+    written back at the end of every group's bin."""
+    _run(lib, torch_dev, n, opt, workgroups, resident,
+         key_group=[k % 3 for k in range(len(KEYS))])
