@@ -530,16 +530,17 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
     }
     DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
     tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
-    int32_t t_stash = tb;  // first tile whose state waits in the stash
+    int32_t t_stash = tb;  // burst write-back: first tile whose state waits in the stash
     for (int32_t t = tb;; ++t) {
         const bool has_next = t < last;
         const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
         uint64_t nprow = 0;
         if constexpr (PULL) nprow = load_row<NW>(outs + int64_t(nd.key) * NW);
         const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
+        PHUB_LDS f4* tile_stash = nullptr;  // this tile's slot of the stash
+        if constexpr (kStash<NW, S, RES, PULL>) tile_stash = stash + (t - t_stash) * kStashTileVecs<S>;
         tile_steps<NW, OPT, RES, PULL>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
-                                       a, b, nd, nrow, prow, has_next, state, o,
-                                       stash + (t - t_stash) * kStashTileVecs<S>);
+                                       a, b, nd, nrow, prow, has_next, state, o, tile_stash);
         if constexpr (kStash<NW, S, RES, PULL>) {
             if (t - t_stash == kStashTiles<S> - 1 || !has_next) {
                 write_stash<NW, S>(tiles, t_stash, t, stash, state);
