@@ -313,16 +313,16 @@ constexpr int kRing = kAhead<NW, S, RES> + 1;
 // LDS, and every kStashTiles tiles the wave writes the stash back in one run
 // of stores.  A few write streams spread evenly through many read streams
 // cost HBM much more than the same bytes written in runs (measured on
-// MI355X with nothing cached: momentum with 13 and 16 workers 0.722 -> 0.753
-// and 0.716 -> 0.774 of peak; plain SGD with 8, 11 and 14 workers 0.763 ->
-// 0.804, 0.743 -> 0.821 and 0.735 -> 0.832).  With fewer gradient streams
-// per state stream the run of stores holds up the wave's load window about
-// as long as it saves or longer (five per state array: within about a point
-// either way; momentum with 7 workers 0.767 -> 0.729, Adam with 12 workers
-// 0.740 -> 0.708), so there the state is written piece by piece.  Only
-// measured with the ring of six, so tied to it.  Each lane reads back only
-// the values it wrote, so the stash needs no barrier.  The stash takes the
-// compute unit's 160 KB of LDS (at most 40 KB per wave).
+// MI355X with nothing cached, fraction of peak: momentum with 12, 14 and 16
+// workers 0.709 -> 0.718, 0.681 -> 0.703 and 0.716 -> 0.774; plain SGD with
+// 10, 14 and 16 workers 0.683 -> 0.745, 0.735 -> 0.832 and 0.653 -> 0.737).
+// With fewer gradient streams per state stream the run of stores holds up
+// the wave's load window for about as long as it saves or longer (five per
+// state array: within about a point either way; momentum with 7 workers
+// 0.767 -> 0.729, Adam with 12 workers 0.740 -> 0.708), so there the state
+// is written piece by piece.  Each lane reads back only the values it
+// wrote, so the stash needs no barrier.  The stash takes the compute unit's
+// 160 KB of LDS (at most 40 KB per wave).
 constexpr int kLdsBytes = 160 * 1024;
 constexpr int kStashBytesPerWave =
     kLdsBytes / kWavesPerBlock < 40 * 1024 ? kLdsBytes / kWavesPerBlock : 40 * 1024;
@@ -336,7 +336,7 @@ constexpr int kStashTileVecs = S * kVecPerLane * 64;
 
 template <int NW, int S, bool RES, bool PULL>
 constexpr bool kStash =
-    !RES && !PULL && kShallowAhead<NW, S> == 5 && NW > 5 * S && kStashTiles<S> >= 2;
+    !RES && !PULL && NW > 5 * S && kStashTiles<S> >= 2;
 
 template <int NW, int S, bool RES, int I>
 __device__ __forceinline__ f4 tile_load(const TileStreams<NW, S>& s) {

@@ -6,8 +6,7 @@ The step is HBM-bound, so its kernels must keep every value in registers:
 no scratch memory, no spilled vector registers, and no LDS (a stray LDS
 copy of the launch scalars once cost plain SGD 3-6 points) except the
 burst write-back stash of the streamed bin, in exactly the fixed-N kernels
-that have it: those without pushpull whose window is a ring of six loads
-(4(N + S) a multiple of 6, S state arrays) and whose N exceeds 5 S,
+that have it: those without pushpull whose N exceeds 5 S (S state arrays),
 each wave holding as many tiles' state as fit 40 KB (4 waves per block).
 The gradient loads must keep the non-temporal hint (gradients are read
 once), and the fixed-N kernels must fit one wave per SIMD.
@@ -51,21 +50,23 @@ def _stash_lds(name):
         return 0
     nw, opt, pull = int(m.group(1)), int(m.group(2)), m.group(3) == "1"
     s = {0: 2, 1: 2, 2: 1, 3: 3}[opt]
-    if pull or (4 * (nw + s)) % 6 or nw <= 5 * s:
+    if pull or nw <= 5 * s:
         return 0
     tiles = (40 * 1024) // (s * 4 * 1024)
     return 4 * tiles * s * 4 * 1024
 
 
 def test_stash_rule_covers_the_measured_cases():
-    # momentum / Nesterov with 13 and 16 workers, plain SGD with 8, 11 and 14;
-    # never Adam, never with pushpull
+    # momentum / Nesterov with 11-16 workers, plain SGD with 6-16, Adam with
+    # 16; never with pushpull
     with_stash = sorted((nw, opt) for nw in range(1, 17) for opt in range(4)
                         if _stash_lds(f"fused_step_fixedILi{nw}ELi{opt}ELb0E"))
-    assert with_stash == [(8, 2), (11, 2), (13, 0), (13, 1), (14, 2), (16, 0), (16, 1)]
+    assert with_stash == sorted([(n, o) for n in range(11, 17) for o in (0, 1)] +
+                                [(n, 2) for n in range(6, 17)] + [(16, 3)])
     assert _stash_lds("fused_step_fixedILi16ELi1ELb0E") == 160 * 1024
     assert _stash_lds("fused_step_fixedILi8ELi2ELb0E") == 160 * 1024
     assert _stash_lds("fused_step_fixedILi10ELi1ELb0E") == 0
+    assert _stash_lds("fused_step_fixedILi16ELi3ELb0E") == 144 * 1024
     assert _stash_lds("fused_step_fixedILi16ELi1ELb1E") == 0
 
 

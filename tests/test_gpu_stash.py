@@ -18,11 +18,13 @@ pytestmark = pytest.mark.gpu
 
 LR, MU, WD, B1, B2, EPS = 0.05, 0.9, 1e-3, 0.9, 0.999, 1e-8
 
-# (workers, optimizer) of the kernels that stash: momentum and Nesterov with
-# 13 and 16 workers, plain SGD with 8, 11 and 14; and, next to them, counts
-# just below the rule (10 momentum, 5 SGD, 15 Adam) that write piece by piece
-STASHED = [(13, "momentum"), (13, "nesterov"), (16, "nesterov"), (16, "momentum"),
-           (8, "sgd"), (11, "sgd"), (14, "sgd"), (10, "momentum"), (5, "sgd"), (15, "adam")]
+# (workers, optimizer): kernels that stash (N > 5 S: momentum and Nesterov
+# with 11-16 workers, plain SGD with 6-16, Adam with 16), and, next to them,
+# counts at the rule's edge (10 momentum, 5 SGD, 15 Adam) that write piece by
+# piece
+STASHED = [(11, "momentum"), (12, "nesterov"), (13, "momentum"), (14, "nesterov"),
+           (15, "momentum"), (16, "nesterov"), (16, "momentum"), (6, "sgd"), (8, "sgd"),
+           (11, "sgd"), (16, "sgd"), (16, "adam"), (10, "momentum"), (5, "sgd"), (15, "adam")]
 # 107 full tiles and ragged ends: a wave of a 1-workgroup grid (4 waves)
 # walks about 27 tiles
 KEYS = (5, 1024 * 37 + 3, 70001, 1024 * 11, 4097, 1, 1024 * 6)
