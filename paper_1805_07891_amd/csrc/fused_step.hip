@@ -26,8 +26,10 @@
 // cut on the host into full tiles and a remainder, so the tile loop is
 // straight-line code.  The tile's loads go out piece by piece in a sliding
 // window that continues into the wave's next tile (see the load window
-// below); each piece is optimized and written back as soon as its last
-// gradient is in.  Gradients are read once per step and loaded
+// below); each piece is optimized as soon as its last gradient is in, and
+// written back at once, or, where the gradient streams far outnumber the
+// state streams, in bursts of several tiles through LDS (the burst
+// write-back below).  Gradients are read once per step and loaded
 // non-temporally.  A wave has two bins: the part of the job whose state is
 // read and written non-temporally like the gradients, and the part whose
 // state stays in the memory-side cache between steps (cache-allocating
