@@ -281,26 +281,41 @@ __device__ __forceinline__ void tile_streams(TileStreams<NW, S>& s, const DevTil
 // of loads in flight must divide the tile's loads, so that every load keeps
 // its register slot from one tile to the next.  Its depth follows the state
 // policy (measured on MI355X):
-//  - non-temporal state: a shallow window, with the state reads and writes
-//    spread through the tile.  Loads and stores share one in-order counter,
-//    so a load issued after a state store is consumed only once that store
-//    has completed, and the depth sets the time a store gets.  Five loads
-//    ahead (a ring of 6) is 1-2 points better than three, for every worker
-//    count it divides the tile of; deeper windows (7 to 35 ahead) are no
-//    better or worse, as they flood the memory system with open streams.
-//    Where a ring of 6 does not divide the tile, three ahead;
+//  - non-temporal state: a short ring of 4 to 8 loads, chosen per worker
+//    count and optimizer from a sweep of every ring that divides the tile
+//    (kRingTable; fraction of peak with nothing cached, ResNet-269-shaped
+//    keys).  A ring of 6 is best wherever it divides the tile (momentum
+//    with 16 workers: 0.769 against 0.718 with a ring of 4 and 0.710 with
+//    8), except Adam with 3 workers (8: 0.760, 6: 0.684); elsewhere 5, 7 or
+//    8 mostly beat 4 (plain SGD with 7 workers: 8 gives 0.793, 4 gives
+//    0.711; Adam with 1 worker 0.724 against 0.600), but not always
+//    (momentum with 5 workers: 4 gives 0.763, 7 gives 0.751).  Loads and
+//    stores share one in-order counter, so where state stores are spread
+//    through the tile a load issued after one is consumed only once it has
+//    completed, and deeper windows flood the memory system with open
+//    streams;
 //  - state held in the memory-side cache: a whole tile ahead (every load of
 //    the next tile in flight while this one is consumed), since only the
 //    gradient streams then reach HBM.
 template <int NW, int S>
 constexpr int kTileLoads = kVecPerLane * (NW + S);
 
+// Ring of the non-temporal window, [S - 1][N - 1] (S = 1 plain SGD, 2
+// momentum, 3 Adam); each entry divides 4 (N + S).  Where two rings
+// measured within half a point, the shorter one.
+constexpr int kRingTable[3][16] = {
+    {8, 6, 8, 5, 6, 7, 8, 6, 8, 4, 6, 4, 7, 6, 8, 4},
+    {6, 8, 5, 6, 4, 4, 6, 5, 4, 6, 4, 7, 6, 8, 4, 6},
+    {8, 5, 8, 7, 8, 6, 8, 4, 6, 4, 7, 6, 8, 4, 6, 4},
+};
+
 #ifdef PHUB_LOADS_AHEAD
 template <int NW, int S>
 constexpr int kShallowAhead = PHUB_LOADS_AHEAD;  // a fixed depth, for sweeps
 #else
 template <int NW, int S>
-constexpr int kShallowAhead = kTileLoads<NW, S> % 6 == 0 ? 5 : 3;
+constexpr int kShallowAhead =
+    (NW >= 1 && NW <= 16 && S >= 1 && S <= 3 ? kRingTable[S - 1][NW - 1] : 4) - 1;
 #endif
 
 template <int NW, int S, bool RES>
