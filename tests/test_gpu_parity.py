@@ -523,6 +523,54 @@ def test_full_size_workload_sampled(lib, torch_dev, name, own_streams):
     torch.cuda.empty_cache()
 
 
+def test_key_past_four_gib_sampled(lib, torch_dev):
+    """One key of 1.2 G elements (4.8 GB per array, the largest size here):
+    element offsets past 2^32 bytes inside a key, the 16 MB folds of the
+    kernel's 32-bit lane offsets, and both bins (the cache budget ends
+    inside the key).  Two steps; sampled elements (each key's ends, around
+    2^30 elements, around the folds and the budget's cut, random) checked
+    bit for bit against the oracle."""
+    torch, dev = torch_dev
+    big = 1_200_000_003
+    keys = (5, big, 1027)
+    spec = Job("large", 2, keys)
+    resident_elems = 3_000_000
+    _say("key of", big, "elements, resident", resident_elems)
+    job = TorchJob(spec, dev, lib=lib, resident_bytes=8 * resident_elems)
+    assert 0.0 < job.cached_fraction() < 0.01
+    _, total = key_offsets(keys)
+    w0 = workloads.device_normal_arena(torch, dev, 7, total, 0.05)
+    job.set_weights(w0)
+    grads = [[workloads.device_normal_arena(torch, dev, 100 + 10 * t + w, total, 1e-2)
+              for w in range(2)] for t in range(2)]
+    for t in range(2):
+        for w in range(2):
+            job.attach_grads(w, grads[t][w])
+        job.push_and_step()
+    W, M = job.state_arenas()
+    pos = set()
+    for k, n in enumerate(keys):
+        pos.update((k, i) for i in list(range(min(n, 3))) + list(range(max(0, n - 5), n)))
+    near = [1 << 30, resident_elems - job.offsets[1]] + [m << 22 for m in (1, 2, 255, 256, 286)]
+    for c in near:
+        pos.update((1, i) for i in range(c - 3, c + 4) if 0 <= i < big)
+    rng = np.random.default_rng(11)
+    pos.update((1, int(i)) for i in rng.integers(0, big, size=20000))
+    idx = np.array(sorted(job.offsets[k] + i for k, i in pos), dtype=np.int64)
+    tidx = torch.from_numpy(idx).to(dev)
+    ws = w0.index_select(0, tidx).cpu().numpy()
+    ms = np.zeros_like(ws)
+    for t in range(2):
+        gs = [grads[t][w].index_select(0, tidx).cpu().numpy() for w in range(2)]
+        oracle.step_flat(gs, ws, ms, spec.lr, spec.momentum, spec.weight_decay, spec.nesterov)
+    _say(f"  {idx.size} sampled elements; W rel err {_rel_err(W[idx], ws):.3g}")
+    assert _bits_equal(W[idx], ws), "W mismatch"
+    assert _bits_equal(M[idx], ms), "M mismatch"
+    job.destroy()
+    del grads, W, M
+    torch.cuda.empty_cache()
+
+
 def test_jobs_driven_from_several_threads(lib, torch_dev):
     """Different jobs may be driven from different threads: each thread
     creates its own job (claiming from the shared cache budget), steps it
