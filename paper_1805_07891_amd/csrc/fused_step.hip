@@ -353,7 +353,7 @@ constexpr int kStashTileVecs = S * kVecPerLane * 64;
 
 template <int NW, int S, bool RES, bool PULL>
 constexpr bool kStash =
-    !RES && !PULL && NW > 5 * S && kStashTiles<S> >= 2;
+    !RES && !PULL && burst_write_back(NW, S) && kStashTiles<S> >= 2;
 
 template <int NW, int S, bool RES, int I>
 __device__ __forceinline__ f4 tile_load(const TileStreams<NW, S>& s) {

@@ -55,6 +55,17 @@ enum OptKind : int {
     kOptAdam = 3,      // Adam with bias correction (state W, M, V)
 };
 
+// Worker counts 1 .. kMaxFixedWorkers have a compile-time kernel each; more
+// workers take the any-N kernel.
+constexpr int kMaxFixedWorkers = 16;
+
+// Whether a fixed-N fused pass (without pushpull) writes the streamed bin's
+// state back in bursts through LDS: where the gradient streams exceed five
+// per state array.  num_states: 1 plain SGD, 2 momentum, 3 Adam.
+constexpr bool burst_write_back(int num_workers, int num_states) {
+    return num_workers >= 1 && num_workers <= kMaxFixedWorkers && num_workers > 5 * num_states;
+}
+
 // Scalars of one launch.  For Adam, c1 = 1 - b1, c2 = 1 - b2 and the
 // step's bias corrections k1 = lr / (1 - b1^t), k2 = 1 / (1 - b2^t) are
 // computed on the host in double and rounded to fp32 once.

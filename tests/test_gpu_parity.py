@@ -319,6 +319,15 @@ def test_default_cache_budget_is_shared(lib, torch_dev):
         tiny = TorchJob(Job("budget.tiny", 1, (1000,)), dev, lib=lib)
         assert tiny.cached_fraction() == 1.0
         tiny.destroy()
+        # plain SGD with 6-16 workers (burst write-back) takes none of the
+        # default budget; with 5 workers, or 17 (the any-N kernel), it does
+        for n, want in ((6, 0.0), (16, 0.0), (5, 1.0), (17, 1.0)):
+            sgd = TorchJob(Job("budget.sgd", n, (1000,)), dev, lib=lib, optimizer="sgd")
+            assert sgd.cached_fraction() == want, n
+            sgd.destroy()
+        sgd = TorchJob(Job("budget.sgd", 8, (1000,)), dev, lib=lib, optimizer="sgd", unfused=True)
+        assert sgd.cached_fraction() == 1.0
+        sgd.destroy()
         # an explicit budget that ends inside the key: cut at a tile boundary
         f = TorchJob(spec, dev, lib=lib, resident_bytes=8 * 5000)
         assert f.info()[4] == 8 * 4096
