@@ -303,7 +303,7 @@ constexpr int kTileLoads = kVecPerLane * (NW + S);
 // Ring of the non-temporal window, [S - 1][N - 1] (S = 1 plain SGD, 2
 // momentum, 3 Adam); each entry divides 4 (N + S).  Where two rings
 // measured within half a point, the shorter one.
-constexpr int kRingTable[3][16] = {
+constexpr int kRingTable[3][kMaxFixedWorkers] = {
     {8, 6, 8, 5, 6, 7, 8, 6, 8, 4, 6, 4, 7, 6, 8, 4},
     {6, 8, 5, 6, 4, 4, 6, 5, 4, 6, 4, 7, 6, 8, 4, 6},
     {8, 5, 8, 7, 8, 6, 8, 4, 6, 4, 7, 6, 8, 4, 6, 4},
@@ -315,7 +315,7 @@ constexpr int kShallowAhead = PHUB_LOADS_AHEAD;  // a fixed depth, for sweeps
 #else
 template <int NW, int S>
 constexpr int kShallowAhead =
-    (NW >= 1 && NW <= 16 && S >= 1 && S <= 3 ? kRingTable[S - 1][NW - 1] : 4) - 1;
+    (NW >= 1 && NW <= kMaxFixedWorkers && S >= 1 && S <= 3 ? kRingTable[S - 1][NW - 1] : 4) - 1;
 #endif
 
 template <int NW, int S, bool RES>
@@ -330,9 +330,10 @@ constexpr int kRing = kAhead<NW, S, RES> + 1;
 // LDS, and every kStashTiles tiles the wave writes the stash back in one run
 // of stores.  A few write streams spread evenly through many read streams
 // cost HBM much more than the same bytes written in runs (measured on
-// MI355X with nothing cached, fraction of peak: momentum with 12, 14 and 16
-// workers 0.709 -> 0.718, 0.681 -> 0.703 and 0.716 -> 0.774; plain SGD with
-// 10, 14 and 16 workers 0.683 -> 0.745, 0.735 -> 0.832 and 0.653 -> 0.737).
+// MI355X with nothing cached and rings of 4 or 6 loads, fraction of peak:
+// momentum with 12, 14 and 16 workers 0.709 -> 0.718, 0.681 -> 0.703 and
+// 0.716 -> 0.774; plain SGD with 10, 14 and 16 workers 0.683 -> 0.745,
+// 0.735 -> 0.832 and 0.653 -> 0.737).
 // With fewer gradient streams per state stream the run of stores holds up
 // the wave's load window for about as long as it saves or longer (five per
 // state array: within about a point either way; momentum with 7 workers
@@ -843,6 +844,7 @@ hipError_t launch_one(const StepParams& p, int grid, hipStream_t stream) {
 
 template <int OPT, bool PULL>
 hipError_t launch_pull(const StepParams& p, int grid, hipStream_t stream) {
+    static_assert(kMaxFixedWorkers == 16, "one case per fixed worker count");
     switch (p.num_workers) {
         case 1: return launch_one<1, OPT, PULL>(p, grid, stream);
         case 2: return launch_one<2, OPT, PULL>(p, grid, stream);
