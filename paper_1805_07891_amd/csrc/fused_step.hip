@@ -48,6 +48,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 #include <utility>
 
 #include "kernels.hpp"
@@ -277,23 +278,22 @@ __device__ __forceinline__ void tile_streams(TileStreams<NW, S>& s, const DevTil
 // Issue order of a tile's loads: for each of the kVecPerLane pieces, the S
 // state arrays (W first), then the gradients in worker order; kTileLoads
 // loads per tile.  A wave keeps a window of loads in flight beyond the one
-// it waits for, and the window runs on into the wave's next tile.  The ring
-// of loads in flight must divide the tile's loads, so that every load keeps
-// its register slot from one tile to the next.  Its depth follows the state
-// policy (measured on MI355X):
-//  - non-temporal state: a short ring of 4 to 8 loads, chosen per worker
-//    count and optimizer from a sweep of every ring that divides the tile
-//    (kRingTable; fraction of peak with nothing cached, ResNet-269-shaped
-//    keys).  A ring of 6 is best wherever it divides the tile (momentum
-//    with 16 workers: 0.769 against 0.718 with a ring of 4 and 0.710 with
-//    8), except Adam with 3 workers (8: 0.760, 6: 0.684); elsewhere 5, 7 or
-//    8 mostly beat 4 (plain SGD with 7 workers: 8 gives 0.793, 4 gives
-//    0.711; Adam with 1 worker 0.724 against 0.600), but not always
-//    (momentum with 5 workers: 4 gives 0.763, 7 gives 0.751).  Loads and
-//    stores share one in-order counter, so where state stores are spread
-//    through the tile a load issued after one is consumed only once it has
-//    completed, and deeper windows flood the memory system with open
-//    streams;
+// it waits for, and the window runs on into the wave's next tile.  Load j
+// of a tile sits in ring slot j mod R; where the ring R does not divide the
+// tile's loads, consecutive tiles take turns (phases) so that every load
+// keeps its slot.  The depth follows the state policy (measured on MI355X):
+//  - non-temporal state: a ring of 6 loads (five ahead), or 5 or 8 for a
+//    few worker counts and optimizers (kRingTable), from a sweep of rings 4
+//    to 8 for every worker count and optimizer (fraction of peak with
+//    nothing cached, ResNet-269-shaped keys).  Six beats four everywhere
+//    (momentum with 16 workers 0.765 against 0.717, plain SGD with 16 0.834
+//    against 0.736, Adam with 10 0.731 against 0.673); eight is better for
+//    Adam with 3-7 workers (3 workers: 0.752 against 0.684) and plain SGD
+//    with 2, 3 or 6; five for momentum with 3 or 8 workers (8: 0.749
+//    against 0.737).  Deeper windows flood the memory system with open
+//    streams, and loads and stores share one in-order counter, so a load
+//    issued after a state store is consumed only once that store has
+//    completed;
 //  - state held in the memory-side cache: a whole tile ahead (every load of
 //    the next tile in flight while this one is consumed), since only the
 //    gradient streams then reach HBM.
@@ -301,12 +301,13 @@ template <int NW, int S>
 constexpr int kTileLoads = kVecPerLane * (NW + S);
 
 // Ring of the non-temporal window, [S - 1][N - 1] (S = 1 plain SGD, 2
-// momentum, 3 Adam); each entry divides 4 (N + S).  Where two rings
-// measured within half a point, the shorter one.
+// momentum, 3 Adam): 6 unless another ring measured more than half a point
+// better.  A ring of 5 must divide the tile's 4 (N + S) loads; 6 and 8 take
+// at most three and two phases.
 constexpr int kRingTable[3][kMaxFixedWorkers] = {
-    {8, 6, 8, 5, 6, 7, 8, 6, 8, 4, 6, 4, 7, 6, 8, 4},
-    {6, 8, 5, 6, 4, 4, 6, 5, 4, 6, 4, 7, 6, 8, 4, 6},
-    {8, 5, 8, 7, 8, 6, 8, 4, 6, 4, 7, 6, 8, 4, 6, 4},
+    {6, 8, 8, 6, 6, 8, 6, 6, 6, 6, 6, 6, 6, 6, 6, 6},
+    {6, 6, 5, 6, 6, 6, 6, 5, 6, 6, 6, 6, 6, 6, 6, 6},
+    {6, 6, 8, 8, 8, 8, 8, 6, 6, 6, 6, 6, 6, 6, 6, 6},
 };
 
 #ifdef PHUB_LOADS_AHEAD
@@ -323,6 +324,14 @@ constexpr int kAhead = RES ? kTileLoads<NW, S> - 1 : kShallowAhead<NW, S>;
 
 template <int NW, int S, bool RES>
 constexpr int kRing = kAhead<NW, S, RES> + 1;
+
+constexpr int gcd_int(int a, int b) { return b == 0 ? a : gcd_int(b, a % b); }
+
+// Where the ring does not divide the tile's loads, a wave's tiles take
+// kPhases turns: load j of a tile in phase h sits in ring slot
+// (h L + j) mod R, and after kPhases tiles the slots line up again.
+template <int NW, int S, bool RES>
+constexpr int kPhases = kRing<NW, S, RES> / gcd_int(kTileLoads<NW, S>, kRing<NW, S, RES>);
 
 // Burst write-back of the streamed bin's state.  Where the gradient streams
 // far outnumber the state streams, the streamed bin does not write a
@@ -380,7 +389,7 @@ struct TilePipe {
 // load of the next tile is issued, the next tile's streams are formed from
 // its descriptor and pointer row, which were fetched at the start of this
 // tile.
-template <int NW, int OPT, bool RES, bool PULL, int I>
+template <int NW, int OPT, bool RES, bool PULL, int PH, int I>
 __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
                                           const TileStreams<NW, kStates<OPT>>& a,
                                           TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
@@ -391,14 +400,15 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
     constexpr int L = kTileLoads<NW, S>;
     constexpr int R = kRing<NW, S, RES>;
     constexpr int J = I + kAhead<NW, S, RES>;
+    constexpr int base = (PH * L) % R;  // slot of this tile's first load
     if constexpr (J < L) {
-        p.ring[J % R] = tile_load<NW, S, RES, J>(a);
+        p.ring[(base + J) % R] = tile_load<NW, S, RES, J>(a);
     } else {
         if constexpr (J == L) tile_streams<NW, S>(b, nd, nrow, state);
-        if (has_next) p.ring[J % R] = tile_load<NW, S, RES, J - L>(b);
+        if (has_next) p.ring[(base + J) % R] = tile_load<NW, S, RES, J - L>(b);
     }
     __builtin_amdgcn_sched_barrier(0);
-    const f4 v = p.ring[I % R];
+    const f4 v = p.ring[(base + I) % R];
     constexpr int k = I % (NW + S);
     constexpr int u = I / (NW + S);
     if constexpr (k < S)
@@ -434,7 +444,7 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
     __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int NW, int OPT, bool RES, bool PULL, int... I>
+template <int NW, int OPT, bool RES, bool PULL, int PH, int... I>
 __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>,
                                            TilePipe<NW, kStates<OPT>, RES>& p,
                                            const TileStreams<NW, kStates<OPT>>& a,
@@ -442,7 +452,7 @@ __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>,
                                            uint64_t nrow, uint64_t prow, bool has_next,
                                            float* const* state, OptArgs o,
                                            PHUB_LDS f4* tile_stash) {
-    (tile_step<NW, OPT, RES, PULL, I>(p, a, b, nd, nrow, prow, has_next, state, o, tile_stash),
+    (tile_step<NW, OPT, RES, PULL, PH, I>(p, a, b, nd, nrow, prow, has_next, state, o, tile_stash),
      ...);
 }
 
@@ -534,8 +544,8 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
                                            float* const* __restrict__ outs, float* const* state,
                                            OptArgs o, PHUB_LDS f4* stash) {
     constexpr int S = kStates<OPT>;
-    static_assert(kTileLoads<NW, S> % kRing<NW, S, RES> == 0,
-                  "the load window must wrap with the tile");
+    constexpr int NPH = kPhases<NW, S, RES>;
+    static_assert(NPH >= 1 && NPH <= 3, "the tile loop below unrolls at most three phases");
     if (tb >= te) return;
     const int32_t last = te - 1;
     TilePipe<NW, S, RES> p;
@@ -549,7 +559,10 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
     DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
     tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
     int32_t t_stash = tb;  // burst write-back: first tile whose state waits in the stash
-    for (int32_t t = tb;; ++t) {
+    int32_t t = tb;
+    // Tile t in ring phase PH; false after the bin's last tile.
+    auto one_tile = [&](auto phase) -> bool {
+        constexpr int PH = decltype(phase)::value;
         const bool has_next = t < last;
         const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
         uint64_t nprow = 0;
@@ -557,18 +570,27 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
         const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
         PHUB_LDS f4* tile_stash = nullptr;  // this tile's slot of the stash
         if constexpr (kStash<NW, S, RES, PULL>) tile_stash = stash + (t - t_stash) * kStashTileVecs<S>;
-        tile_steps<NW, OPT, RES, PULL>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
-                                       a, b, nd, nrow, prow, has_next, state, o, tile_stash);
+        tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
+                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash);
         if constexpr (kStash<NW, S, RES, PULL>) {
             if (t - t_stash == kStashTiles<S> - 1 || !has_next) {
                 write_stash<NW, S>(tiles, t_stash, t, stash, state);
                 t_stash = t + 1;
             }
         }
-        if (!has_next) break;
+        if (!has_next) return false;
         a = b;
         nd = nd2;
         prow = nprow;
+        ++t;
+        return true;
+    };
+    for (;;) {
+        if (!one_tile(std::integral_constant<int, 0>{})) break;
+        if constexpr (NPH >= 2)
+            if (!one_tile(std::integral_constant<int, 1 % NPH>{})) break;
+        if constexpr (NPH >= 3)
+            if (!one_tile(std::integral_constant<int, 2 % NPH>{})) break;
     }
 }
 
@@ -832,8 +854,7 @@ hipError_t launch_any(const StepParams& p, int grid, hipStream_t stream) {
 template <int NW, int OPT, bool PULL>
 hipError_t launch_one(const StepParams& p, int grid, hipStream_t stream) {
     constexpr int S = kStates<OPT>;
-    if constexpr (kTileLoads<NW, S> % kRing<NW, S, true> == 0 &&
-                  kTileLoads<NW, S> % kRing<NW, S, false> == 0) {
+    if constexpr (kPhases<NW, S, true> <= 3 && kPhases<NW, S, false> <= 3) {
         hipLaunchKernelGGL((fused_step_fixed<NW, OPT, PULL>), dim3(grid), dim3(kBlockThreads), 0,
                            stream, PHUB_LAUNCH_ARGS);
         return hipGetLastError();
