@@ -316,16 +316,27 @@ constexpr int kShallowAhead = PHUB_LOADS_AHEAD;  // a fixed depth, for sweeps
 #else
 template <int NW, int S>
 constexpr int kShallowAhead =
-    (NW >= 1 && NW <= kMaxFixedWorkers && S >= 1 && S <= 3 ? kRingTable[S - 1][NW - 1] : 4) - 1;
+    (NW >= 1 && NW <= kMaxFixedWorkers && S >= 1 && S <= 3 ? kRingTable[S - 1][NW - 1] : 6) - 1;
 #endif
 
+constexpr int gcd_int(int a, int b) { return b == 0 ? a : gcd_int(b, a % b); }
+
+// Ring of the resident bin: a whole tile while that fits the registers
+// (up to 80 loads, 320 VGPRs); beyond, the largest of 32, 24, 20, 16 loads
+// that needs at most three phases (rings of 12 or 24 measured equal to the
+// whole tile at 8-16 workers).
+constexpr int resident_ring(int loads) {
+    if (loads <= 80) return loads;
+    for (int r : {32, 24, 20, 16})
+        if (r / gcd_int(loads, r) <= 3) return r;
+    return 4;
+}
+
 template <int NW, int S, bool RES>
-constexpr int kAhead = RES ? kTileLoads<NW, S> - 1 : kShallowAhead<NW, S>;
+constexpr int kAhead = RES ? resident_ring(kTileLoads<NW, S>) - 1 : kShallowAhead<NW, S>;
 
 template <int NW, int S, bool RES>
 constexpr int kRing = kAhead<NW, S, RES> + 1;
-
-constexpr int gcd_int(int a, int b) { return b == 0 ? a : gcd_int(b, a % b); }
 
 // Where the ring does not divide the tile's loads, a wave's tiles take
 // kPhases turns: load j of a tile in phase h sits in ring slot
@@ -866,6 +877,8 @@ hipError_t launch_one(const StepParams& p, int grid, hipStream_t stream) {
 template <int OPT, bool PULL>
 hipError_t launch_pull(const StepParams& p, int grid, hipStream_t stream) {
     static_assert(kMaxFixedWorkers == 16, "one case per fixed worker count");
+    static_assert(has_fixed_kernel(20) && has_fixed_kernel(24) && has_fixed_kernel(32),
+                  "the larger counts below");
     switch (p.num_workers) {
         case 1: return launch_one<1, OPT, PULL>(p, grid, stream);
         case 2: return launch_one<2, OPT, PULL>(p, grid, stream);
@@ -883,6 +896,9 @@ hipError_t launch_pull(const StepParams& p, int grid, hipStream_t stream) {
         case 14: return launch_one<14, OPT, PULL>(p, grid, stream);
         case 15: return launch_one<15, OPT, PULL>(p, grid, stream);
         case 16: return launch_one<16, OPT, PULL>(p, grid, stream);
+        case 20: return launch_one<20, OPT, PULL>(p, grid, stream);
+        case 24: return launch_one<24, OPT, PULL>(p, grid, stream);
+        case 32: return launch_one<32, OPT, PULL>(p, grid, stream);
         default: return launch_any<OPT, PULL>(p, grid, stream);
     }
 }

@@ -55,15 +55,20 @@ enum OptKind : int {
     kOptAdam = 3,      // Adam with bias correction (state W, M, V)
 };
 
-// Worker counts 1 .. kMaxFixedWorkers have a compile-time kernel each; more
-// workers take the any-N kernel.
+// Worker counts 1 .. kMaxFixedWorkers, and 20, 24 and 32, have a
+// compile-time kernel each; other counts take the any-N kernel.
 constexpr int kMaxFixedWorkers = 16;
+
+constexpr bool has_fixed_kernel(int num_workers) {
+    return (num_workers >= 1 && num_workers <= kMaxFixedWorkers) || num_workers == 20 ||
+           num_workers == 24 || num_workers == 32;
+}
 
 // Whether a fixed-N fused pass (without pushpull) writes the streamed bin's
 // state back in bursts through LDS: where the gradient streams exceed five
 // per state array.  num_states: 1 plain SGD, 2 momentum, 3 Adam.
 constexpr bool burst_write_back(int num_workers, int num_states) {
-    return num_workers >= 1 && num_workers <= kMaxFixedWorkers && num_workers > 5 * num_states;
+    return has_fixed_kernel(num_workers) && num_workers > 5 * num_states;
 }
 
 // Scalars of one launch.  For Adam, c1 = 1 - b1, c2 = 1 - b2 and the

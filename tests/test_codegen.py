@@ -50,7 +50,7 @@ def _stash_lds(name):
         return 0
     nw, opt, pull = int(m.group(1)), int(m.group(2)), m.group(3) == "1"
     s = {0: 2, 1: 2, 2: 1, 3: 3}[opt]
-    if pull or nw <= 5 * s:
+    if pull or nw <= 5 * s or not (nw <= 16 or nw in (20, 24, 32)):
         return 0
     tiles = (40 * 1024) // (s * 4 * 1024)
     return 4 * tiles * s * 4 * 1024
@@ -73,8 +73,8 @@ def test_stash_rule_covers_the_measured_cases():
 def test_every_kernel_keeps_its_data_in_registers(asm):
     meta = _kernels(asm)
     fixed = [n for n in meta if "fused_step_fixed" in n]
-    # N = 1..16, four optimizer forms, with and without pushpull
-    assert len(fixed) == 16 * 4 * 2
+    # N = 1..16, 20, 24 and 32, four optimizer forms, with and without pushpull
+    assert len(fixed) == 19 * 4 * 2
     assert any("fused_step_any" in n for n in meta)
     assert any("aggregate_only" in n for n in meta) and any("optimize_only" in n for n in meta)
     for name, m in meta.items():

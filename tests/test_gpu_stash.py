@@ -123,3 +123,13 @@ def test_burst_write_back_per_readiness_group(lib, torch_dev, n, opt, workgroups
     written back at the end of every group's bin."""
     _run(lib, torch_dev, n, opt, workgroups, resident,
          key_group=[k % 3 for k in range(len(KEYS))])
+
+
+@pytest.mark.parametrize("n", [20, 24, 32])
+@pytest.mark.parametrize("opt", ["momentum", "nesterov", "sgd", "adam"])
+@pytest.mark.parametrize("workgroups,resident", [(1, 0), (None, "partial")])
+def test_larger_fixed_worker_counts(lib, torch_dev, n, opt, workgroups, resident):
+    """20, 24 and 32 workers have kernels of their own (phased ring of 6,
+    burst write-back, resident ring below a whole tile); bit-exact against
+    the oracle like the others."""
+    _run(lib, torch_dev, n, opt, workgroups, resident)
