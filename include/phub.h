@@ -121,10 +121,10 @@ typedef struct phub_options {
                                come, first served by the live jobs created
                                with -1 (each takes what its state needs of
                                what is left) and given back by phub_destroy;
-                               plain SGD with 6 to 16 workers (not unfused)
-                               takes none of it, since its streamed state is
-                               written back in bursts and streams faster
-                               than it caches.  Results do not depend on
+                               plain SGD with 6 to 16 or 20, 24, 32 workers
+                               and every job with more than 16 workers (not
+                               unfused) take none of it: they stream faster
+                               than they cache.  Results do not depend on
                                it. */
     int num_groups;         /* readiness groups (sections 3.2.2-3.2.3: a
                                chunk is aggregated as soon as all of its

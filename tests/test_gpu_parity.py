@@ -319,12 +319,13 @@ def test_default_cache_budget_is_shared(lib, torch_dev):
         tiny = TorchJob(Job("budget.tiny", 1, (1000,)), dev, lib=lib)
         assert tiny.cached_fraction() == 1.0
         tiny.destroy()
-        # plain SGD with 6-16 workers (burst write-back) takes none of the
-        # default budget; with 5 workers, or 17 (the any-N kernel), it does
-        for n, want in ((6, 0.0), (16, 0.0), (5, 1.0), (17, 1.0)):
-            sgd = TorchJob(Job("budget.sgd", n, (1000,)), dev, lib=lib, optimizer="sgd")
-            assert sgd.cached_fraction() == want, n
-            sgd.destroy()
+        # plain SGD with burst write-back (6-16 workers) and every job with
+        # more than 16 workers take none of the default budget
+        for n, opt, want in ((6, "sgd", 0.0), (16, "sgd", 0.0), (5, "sgd", 1.0), (17, "sgd", 0.0),
+                             (16, None, 1.0), (17, None, 0.0), (32, None, 0.0), (20, "adam", 0.0)):
+            jb = TorchJob(Job("budget.n", n, (1000,)), dev, lib=lib, optimizer=opt)
+            assert jb.cached_fraction() == want, (n, opt)
+            jb.destroy()
         sgd = TorchJob(Job("budget.sgd", 8, (1000,)), dev, lib=lib, optimizer="sgd", unfused=True)
         assert sgd.cached_fraction() == 1.0
         sgd.destroy()
