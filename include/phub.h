@@ -121,8 +121,8 @@ typedef struct phub_options {
                                come, first served by the live jobs created
                                with -1 (each takes what its state needs of
                                what is left) and given back by phub_destroy;
-                               plain SGD with 6 to 16 or 20, 24, 32 workers
-                               and every job with more than 16 workers (not
+                               plain SGD with 6 to 16, 20, 24 or 32 workers
+                               and every job with 20, 24 or 32 workers (not
                                unfused) take none of it: they stream faster
                                than they cache.  Results do not depend on
                                it. */

@@ -679,13 +679,57 @@ __device__ __forceinline__ f4 sum_any(const float* const* kp, int n, int64_t off
     return s;
 }
 
+// The same over kVecPerLane float4 per lane at once (1 KB apart): every
+// batch keeps kBatch * kVecPerLane loads in flight.
+__device__ __forceinline__ void sum_any_pieces(const float* const* kp, int n, int64_t offset,
+                                               uint32_t bo, f4* s) {
+#pragma unroll
+    for (int u = 0; u < kVecPerLane; ++u) s[u] = load_stream(kp[0] + offset, bo + u * 1024u);
+    for (int w0 = 1; w0 < n; w0 += kBatch) {
+        f4 a[kBatch][kVecPerLane];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (w0 + j < n) {
+#pragma unroll
+                for (int u = 0; u < kVecPerLane; ++u)
+                    a[j][u] = load_stream(kp[w0 + j] + offset, bo + u * 1024u);
+            }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (w0 + j < n) {
+#pragma unroll
+                for (int u = 0; u < kVecPerLane; ++u) s[u] = s[u] + a[j][u];
+            }
+    }
+}
+
 template <int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void run_any(const float* const* kp, float* const* ko, int n,
                                         int64_t offset, float* const* stb, uint32_t nvec,
                                         uint32_t rem, OptArgs o) {
     constexpr int S = kStates<OPT>;
     const uint32_t lane = threadIdx.x & 63u;
-    for (uint32_t v = lane; v < nvec; v += 64u) {
+    // whole groups of kVecPerLane * 64 float4 (a full tile is one), then the rest
+    const uint32_t nfull = nvec / (64u * kVecPerLane) * (64u * kVecPerLane);
+    for (uint32_t v = lane; v < nfull; v += 64u * kVecPerLane) {
+        const uint32_t bo = v * 16u;
+        f4 sum[kVecPerLane];
+        sum_any_pieces(kp, n, offset, bo, sum);
+        f4 st[kVecPerLane][S];
+#pragma unroll
+        for (int u = 0; u < kVecPerLane; ++u)
+#pragma unroll
+            for (int i = 0; i < S; ++i) st[u][i] = load_wm<RES>(stb[i], bo + u * 1024u);
+#pragma unroll
+        for (int u = 0; u < kVecPerLane; ++u) {
+            update4<OPT>(sum[u], st[u], o);
+#pragma unroll
+            for (int i = 0; i < S; ++i) store_wm<RES>(stb[i], bo + u * 1024u, st[u][i]);
+            if constexpr (PULL)
+                for (int w = 0; w < n; ++w) store_out(ko[w] + offset, bo + u * 1024u, st[u][0]);
+        }
+    }
+    for (uint32_t v = nfull + lane; v < nvec; v += 64u) {
         const uint32_t bo = v * 16u;
         const f4 s = sum_any(kp, n, offset, bo);
         f4 st[S];

@@ -610,22 +610,22 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     // Cache residency: the state of arena elements [0, resident_elems) is
     // kept in the memory-side cache.  An explicit budget is the job's own;
     // the default takes what is left of the device's shared budget, first
-    // come first served.  Two kinds of job step faster with all of their
-    // state streamed than with part of it cached, and by default leave the
-    // shared budget to other jobs (measured on MI355X, fraction of peak):
-    // plain SGD whose streamed state is written back in bursts (102 M
-    // parameters: 8 workers 0.800 against 0.768, 14 workers 0.830 against
-    // 0.754), and every job with more than 16 workers (ResNet-50's keys:
+    // come first served.  Jobs whose streamed state is written back in
+    // bursts step faster with all of their state streamed than with part of
+    // it cached where they are plain SGD or have more than 16 workers, and
+    // by default leave the shared budget to other jobs (measured on MI355X,
+    // fraction of peak: plain SGD, 102 M parameters, 8 workers 0.800
+    // against 0.768, 14 workers 0.830 against 0.754; ResNet-50's keys,
     // momentum with 20 workers 0.791 against 0.736, Adam 0.751 against
-    // 0.669).
+    // 0.669).  The any-N kernel has no bursts, and caching pays there.
     j->num_states = j->opt == phub::kOptSgd ? 1 : j->opt == phub::kOptAdam ? 3 : 2;
     const int64_t elem_state_bytes = j->num_states * int64_t(sizeof(float));
     {
         std::lock_guard<std::mutex> lk(g_live_mu);
         int64_t budget = resident_bytes;
-        const bool stream_all =
-            !unfused && ((j->opt == phub::kOptSgd && phub::burst_write_back(num_workers, 1)) ||
-                         num_workers > phub::kMaxFixedWorkers);
+        const bool stream_all = !unfused &&
+                                phub::burst_write_back(num_workers, j->num_states) &&
+                                (j->opt == phub::kOptSgd || num_workers > phub::kMaxFixedWorkers);
         if (budget < 0)
             budget = stream_all ? 0 : std::max<int64_t>(0, PHUB_DEVICE_CACHE_BYTES - g_cache_claimed[j->device]);
         j->resident_elems = std::min(j->arena_elems, budget / elem_state_bytes);

@@ -319,10 +319,12 @@ def test_default_cache_budget_is_shared(lib, torch_dev):
         tiny = TorchJob(Job("budget.tiny", 1, (1000,)), dev, lib=lib)
         assert tiny.cached_fraction() == 1.0
         tiny.destroy()
-        # plain SGD with burst write-back (6-16 workers) and every job with
-        # more than 16 workers take none of the default budget
-        for n, opt, want in ((6, "sgd", 0.0), (16, "sgd", 0.0), (5, "sgd", 1.0), (17, "sgd", 0.0),
-                             (16, None, 1.0), (17, None, 0.0), (32, None, 0.0), (20, "adam", 0.0)):
+        # plain SGD with burst write-back (6-16, 20, 24, 32 workers) and every
+        # job with 20, 24 or 32 workers take none of the default budget; the
+        # any-N kernel (17 workers) has no bursts and caches
+        for n, opt, want in ((6, "sgd", 0.0), (16, "sgd", 0.0), (5, "sgd", 1.0), (17, "sgd", 1.0),
+                             (16, None, 1.0), (17, None, 1.0), (32, None, 0.0), (20, "adam", 0.0),
+                             (24, "sgd", 0.0)):
             jb = TorchJob(Job("budget.n", n, (1000,)), dev, lib=lib, optimizer=opt)
             assert jb.cached_fraction() == want, (n, opt)
             jb.destroy()
