@@ -116,7 +116,8 @@ def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups,
     _run(lib, torch_dev, n, opt, workgroups, resident)
 
 
-@pytest.mark.parametrize("n,opt", [(16, "nesterov"), (13, "momentum"), (11, "sgd")])
+@pytest.mark.parametrize("n,opt", [(16, "nesterov"), (13, "momentum"), (11, "sgd"), (24, "momentum"),
+                                   (32, "sgd"), (20, "adam")])
 @pytest.mark.parametrize("workgroups,resident", [(1, 0), (None, "partial")])
 def test_burst_write_back_per_readiness_group(lib, torch_dev, n, opt, workgroups, resident):
     """Each readiness group's launch walks its own tiles: the stash is
