@@ -121,11 +121,12 @@ typedef struct phub_options {
                                come, first served by the live jobs created
                                with -1 (each takes what its state needs of
                                what is left) and given back by phub_destroy;
-                               plain SGD with 6 to 16, 20, 24 or 32 workers
-                               and every job with 20, 24 or 32 workers (not
-                               unfused) take none of it: they stream faster
-                               than they cache.  Results do not depend on
-                               it. */
+                               jobs whose streamed state is written back in
+                               bursts take none of it (they stream as fast as
+                               they cache): momentum SGD and plain SGD with
+                               6 to 16, 20, 24 or 32 workers, Adam with 14 to
+                               16, 20, 24 or 32, not unfused.  Results do not
+                               depend on it. */
     int num_groups;         /* readiness groups (sections 3.2.2-3.2.3: a
                                chunk is aggregated as soon as all of its
                                pieces have arrived).  0: none; the whole step

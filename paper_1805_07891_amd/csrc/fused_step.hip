@@ -27,9 +27,9 @@
 // straight-line code.  The tile's loads go out piece by piece in a sliding
 // window that continues into the wave's next tile (see the load window
 // below); each piece is optimized as soon as its last gradient is in, and
-// written back at once, or, where the gradient streams far outnumber the
-// state streams, in bursts of several tiles through LDS (the burst
-// write-back below).  Gradients are read once per step and loaded
+// written back at once, or, from enough gradient streams per state stream,
+// in bursts of several tiles through LDS, timed by a chip-wide clock so
+// that all waves write together (the burst write-back below).  Gradients are read once per step and loaded
 // non-temporally.  A wave has two bins: the part of the job whose state is
 // read and written non-temporally like the gradients, and the part whose
 // state stays in the memory-side cache between steps (cache-allocating
@@ -302,11 +302,13 @@ constexpr int kTileLoads = kVecPerLane * (NW + S);
 
 // Ring of the non-temporal window, [S - 1][N - 1] (S = 1 plain SGD, 2
 // momentum, 3 Adam): 6 unless another ring measured more than half a point
-// better.  A ring of 5 must divide the tile's 4 (N + S) loads; 6 and 8 take
-// at most three and two phases.
+// better (momentum with 8 workers took 5 before its state was written back
+// in the write phases below; with them, 6 is 5 points faster on a
+// 143.7 M-parameter job).  A ring of 5 must divide the tile's 4 (N + S)
+// loads; 6 and 8 take at most three and two phases.
 constexpr int kRingTable[3][kMaxFixedWorkers] = {
     {6, 8, 8, 6, 6, 8, 6, 6, 6, 6, 6, 6, 6, 6, 6, 6},
-    {6, 6, 5, 6, 6, 6, 6, 5, 6, 6, 6, 6, 6, 6, 6, 6},
+    {6, 6, 5, 6, 6, 6, 6, 6, 6, 6, 6, 6, 6, 6, 6, 6},
     {6, 6, 8, 8, 8, 8, 8, 6, 6, 6, 6, 6, 6, 6, 6, 6},
 };
 
@@ -344,23 +346,28 @@ constexpr int kRing = kAhead<NW, S, RES> + 1;
 template <int NW, int S, bool RES>
 constexpr int kPhases = kRing<NW, S, RES> / gcd_int(kTileLoads<NW, S>, kRing<NW, S, RES>);
 
-// Burst write-back of the streamed bin's state.  Where the gradient streams
-// far outnumber the state streams, the streamed bin does not write a
-// piece's new state as soon as it is computed: the state goes to a stash in
-// LDS, and every kStashTiles tiles the wave writes the stash back in one run
-// of stores.  A few write streams spread evenly through many read streams
-// cost HBM much more than the same bytes written in runs (measured on
-// MI355X with nothing cached and rings of 4 or 6 loads, fraction of peak:
-// momentum with 12, 14 and 16 workers 0.709 -> 0.718, 0.681 -> 0.703 and
-// 0.716 -> 0.774; plain SGD with 10, 14 and 16 workers 0.683 -> 0.745,
-// 0.735 -> 0.832 and 0.653 -> 0.737).
-// With fewer gradient streams per state stream the run of stores holds up
-// the wave's load window for about as long as it saves or longer (five per
-// state array: within about a point either way; momentum with 7 workers
-// 0.767 -> 0.729, Adam with 12 workers 0.740 -> 0.708), so there the state
-// is written piece by piece.  Each lane reads back only the values it
-// wrote, so the stash needs no barrier.  The stash takes the compute unit's
-// 160 KB of LDS (at most 40 KB per wave).
+// Burst write-back of the streamed bin's state, in chip-wide write phases.
+// A few write streams spread evenly through many read streams cost HBM much
+// more than the same bytes written in runs.  So, from enough workers per
+// state array (burst_write_back), the streamed bin does not write a piece's
+// new state as soon as it is computed: the state goes to a stash in LDS,
+// and the wave writes the stash back in one run of stores when it finishes
+// a tile inside the write window, or when the stash is full (kStashTiles
+// tiles), or after its last tile.  The write window is the first part of a
+// period of the device's constant-rate wall clock, which every wave of
+// every launch on the chip reads alike: the waves write at the same time
+// and read at the same time, so HBM sees long runs of writes and long runs
+// of reads instead of a steady mix.  The period follows the tile's bytes
+// (kWritePeriodNsPerStream per stream: about the time a wave takes to fill
+// its stash) and the window is about two tiles long (kWriteWindowNs).
+// Measured on MI355X with nothing cached, fraction of peak (8 workers,
+// momentum): 143.7 M parameters 0.72 -> 0.80, 61.1 M 0.78 -> 0.80, 102 M
+// with 16 workers 0.77 -> 0.82; the same stash flushed only when full,
+// 0.73 on the first; flushed on each compute unit's own cycle counter
+// (not aligned across the chip) with the same period, 0.71.
+// Each lane reads back only the values it wrote, so the stash needs no
+// barrier, and results do not depend on when it is written back.  The
+// stash takes the compute unit's 160 KB of LDS (at most 40 KB per wave).
 constexpr int kLdsBytes = 160 * 1024;
 constexpr int kStashBytesPerWave =
     kLdsBytes / kWavesPerBlock < 40 * 1024 ? kLdsBytes / kWavesPerBlock : 40 * 1024;
@@ -465,6 +472,16 @@ __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>,
                                            PHUB_LDS f4* tile_stash) {
     (tile_step<NW, OPT, RES, PULL, PH, I>(p, a, b, nd, nrow, prow, has_next, state, o, tile_stash),
      ...);
+}
+
+// Whether the device's wall clock is inside a write window of the burst
+// write-back (the same answer for every lane: the clock is a scalar).  The
+// low 32 bits of the clock wrap every 43 s at 100 MHz; the wrap shifts the
+// phase of the periods once, which costs nothing but a slightly misplaced
+// window.
+__device__ __forceinline__ bool in_write_window(uint32_t period, uint32_t window) {
+    const uint32_t now = uint32_t(wall_clock64());
+    return now % period < window;
 }
 
 // Writes back the stashed state of the wave's tiles [t0, t1] (streamed
@@ -584,7 +601,8 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
         tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
                                            a, b, nd, nrow, prow, has_next, state, o, tile_stash);
         if constexpr (kStash<NW, S, RES, PULL>) {
-            if (t - t_stash == kStashTiles<S> - 1 || !has_next) {
+            if (t - t_stash == kStashTiles<S> - 1 || !has_next ||
+                in_write_window(o.wb_period, o.wb_window)) {
                 write_stash<NW, S>(tiles, t_stash, t, stash, state);
                 t_stash = t + 1;
             }

@@ -65,11 +65,27 @@ constexpr bool has_fixed_kernel(int num_workers) {
 }
 
 // Whether a fixed-N fused pass (without pushpull) writes the streamed bin's
-// state back in bursts through LDS: where the gradient streams exceed five
-// per state array.  num_states: 1 plain SGD, 2 momentum, 3 Adam.
+// state back in bursts through LDS, in the chip-wide write phases below:
+// from 6 workers for momentum and plain SGD, from 14 for Adam (measured on
+// MI355X with nothing cached, against piece-by-piece write-back: momentum
+// with 6-16 workers +0.7 to +4.5 points, plain SGD with 6-16 up to +0.8,
+// Adam with 14 and 16 +2.7 and +1.7; with fewer workers 1.5 to 15 points
+// slower).  num_states: 1 plain SGD, 2 momentum, 3 Adam.
+constexpr int kBurstMinWorkers[3] = {6, 6, 14};
+
 constexpr bool burst_write_back(int num_workers, int num_states) {
-    return has_fixed_kernel(num_workers) && num_workers > 5 * num_states;
+    return has_fixed_kernel(num_workers) && num_states >= 1 && num_states <= 3 &&
+           num_workers >= kBurstMinWorkers[num_states - 1];
 }
+
+// Chip-wide write phases of the burst write-back.  Every wave of every
+// launch reads the same constant-rate wall clock; the clock's time is cut
+// into periods, and the first part of each period (the write window) is
+// when waves write back their stashed state.  Period per element stream of
+// a tile (N + 2 S streams: gradients, state read, state written) and
+// window, in nanoseconds; the host converts them to clock ticks.
+constexpr int64_t kWritePeriodNsPerStream = 3200;
+constexpr int64_t kWriteWindowNs = 15360;
 
 // Scalars of one launch.  For Adam, c1 = 1 - b1, c2 = 1 - b2 and the
 // step's bias corrections k1 = lr / (1 - b1^t), k2 = 1 / (1 - b2^t) are
@@ -79,6 +95,10 @@ struct OptArgs {
     float mu;
     float wd;
     float b1, b2, c1, c2, k1, k2, eps;
+    // burst write-back (see kWritePeriodNsPerStream): the write phases'
+    // period and window in ticks of the device's wall clock
+    uint32_t wb_period;
+    uint32_t wb_window;
 };
 
 // The schedule of one launch has two bins per wave.  With

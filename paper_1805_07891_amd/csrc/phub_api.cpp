@@ -103,6 +103,7 @@ struct phub_job {
     int64_t steps_done = 0;         // completed steps (Adam's bias correction)
 
     int device = 0;
+    int64_t wall_clock_khz = 0;  // rate of the device's constant wall clock
     hipStream_t stream = nullptr;
     bool own_stream = false;
 
@@ -292,6 +293,12 @@ phub::OptArgs optimizer_args(const phub_job* j) {
     o.nlr = -j->lr;
     o.mu = j->mu;
     o.wd = j->wd;
+    // write phases of the burst write-back, in wall-clock ticks
+    const int64_t streams = j->num_workers + 2 * int64_t(j->num_states);
+    const int64_t period = phub::kWritePeriodNsPerStream * streams * j->wall_clock_khz / 1000000;
+    const int64_t window = phub::kWriteWindowNs * j->wall_clock_khz / 1000000;
+    o.wb_period = uint32_t(std::min<int64_t>(std::max<int64_t>(period, 2), INT32_MAX));
+    o.wb_window = uint32_t(std::min<int64_t>(std::max<int64_t>(window, 1), o.wb_period - 1));
     if (j->opt == phub::kOptAdam) {
         const double t = double(j->steps_done + 1);
         o.b1 = j->b1;
@@ -606,26 +613,36 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         return e != hipSuccess ? hip_fail(e, "hipDeviceGetAttribute(CU count)")
                                : fail(PHUB_EHIP, "device reports no compute units");
     }
+    int clock_khz = 0;
+    e = hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, j->device);
+    if (e != hipSuccess || clock_khz < 1) {
+        delete j;
+        return e != hipSuccess ? hip_fail(e, "hipDeviceGetAttribute(wall clock rate)")
+                               : fail(PHUB_EHIP, "device reports no wall clock");
+    }
+    j->wall_clock_khz = clock_khz;
 
     // Cache residency: the state of arena elements [0, resident_elems) is
     // kept in the memory-side cache.  An explicit budget is the job's own;
     // the default takes what is left of the device's shared budget, first
     // come first served.  Jobs whose streamed state is written back in
-    // bursts step faster with all of their state streamed than with part of
-    // it cached where they are plain SGD or have more than 16 workers, and
-    // by default leave the shared budget to other jobs (measured on MI355X,
-    // fraction of peak: plain SGD, 102 M parameters, 8 workers 0.800
-    // against 0.768, 14 workers 0.830 against 0.754; ResNet-50's keys,
-    // momentum with 20 workers 0.791 against 0.736, Adam 0.751 against
-    // 0.669).  The any-N kernel has no bursts, and caching pays there.
+    // bursts (burst_write_back) step faster with all of their state
+    // streamed than with part of it cached, and as fast as with all of it
+    // cached once the cache no longer holds it from the previous step, so by
+    // default they take none of the shared budget (measured on MI355X,
+    // fraction of peak, nothing cached against the default: 102 M
+    // parameters with 16 workers 0.82 against 0.79; four concurrent
+    // 8-worker jobs 0.77 against 0.76; 25.6 M parameters with 8 workers
+    // 0.79 streamed, 0.83 cached while the cache keeps the state from the
+    // previous step and 0.75 after the cache was flushed).  Jobs without
+    // bursts (few workers, the any-N kernel, the unfused variant) still gain
+    // from the cache.
     j->num_states = j->opt == phub::kOptSgd ? 1 : j->opt == phub::kOptAdam ? 3 : 2;
     const int64_t elem_state_bytes = j->num_states * int64_t(sizeof(float));
     {
         std::lock_guard<std::mutex> lk(g_live_mu);
         int64_t budget = resident_bytes;
-        const bool stream_all = !unfused &&
-                                phub::burst_write_back(num_workers, j->num_states) &&
-                                (j->opt == phub::kOptSgd || num_workers > phub::kMaxFixedWorkers);
+        const bool stream_all = !unfused && phub::burst_write_back(num_workers, j->num_states);
         if (budget < 0)
             budget = stream_all ? 0 : std::max<int64_t>(0, PHUB_DEVICE_CACHE_BYTES - g_cache_claimed[j->device]);
         j->resident_elems = std::min(j->arena_elems, budget / elem_state_bytes);

@@ -194,6 +194,40 @@ class TorchJob:
         copy_to_host(V, v_ptr)
         return V
 
+    def key_state_pointers(self, key: int):
+        """Device addresses of key ``key``'s state as the library hands them
+        out: (phub_pull's W, phub_get_state's W and M, phub_get_second_moment's
+        V); 0 where the optimizer keeps no such array."""
+        w_pull = self.lib.phub_pull(self.handle, key)
+        w_state, m = self.lib.phub_get_state(self.handle, key)
+        v = self.lib.phub_get_second_moment(self.handle, key)
+        return w_pull, w_state, m, v
+
+    def pulled_keys(self):
+        """Every key's state copied to the host through the per-key pointers
+        of the Pull interface: a list of (W, M, V) per key, W read from
+        phub_pull, M from phub_get_state, V from phub_get_second_moment (None
+        where the optimizer keeps no such array).  Raises if phub_pull and
+        phub_get_state disagree on a key's weights."""
+        self.sync()
+        out = []
+        for k, n in enumerate(self.spec.key_elems):
+            w_pull, w_state, m_ptr, v_ptr = self.key_state_pointers(k)
+            if w_pull != w_state:
+                raise RuntimeError(f"key {k}: phub_pull gives {w_pull:#x}, "
+                                   f"phub_get_state {w_state:#x}")
+            arrays = []
+            for ptr in (w_pull, m_ptr, v_ptr):
+                if not ptr:
+                    arrays.append(None)
+                    continue
+                a = np.empty(n, dtype=np.float32)
+                if n:
+                    copy_to_host(a, ptr)
+                arrays.append(a)
+            out.append(tuple(arrays))
+        return out
+
     def split(self, arena: np.ndarray) -> List[np.ndarray]:
         return [arena[o:o + n] for o, n in zip(self.offsets, self.spec.key_elems)]
 

@@ -6,8 +6,10 @@ The step is HBM-bound, so its kernels must keep every value in registers:
 no scratch memory, no spilled vector registers, and no LDS (a stray LDS
 copy of the launch scalars once cost plain SGD 3-6 points) except the
 burst write-back stash of the streamed bin, in exactly the fixed-N kernels
-that have it: those without pushpull whose N exceeds 5 S (S state arrays),
-each wave holding as many tiles' state as fit 40 KB (4 waves per block).
+that have it: those without pushpull with at least 6 workers for momentum
+and plain SGD, at least 14 for Adam, each wave holding as many tiles' state
+as fit 40 KB (4 waves per block).  Those kernels read the device's wall
+clock (the write phases of the burst write-back) and no other kernel does.
 The gradient loads must keep the non-temporal hint (gradients are read
 once), and the fixed-N kernels must fit one wave per SIMD.
 """
@@ -50,24 +52,33 @@ def _stash_lds(name):
         return 0
     nw, opt, pull = int(m.group(1)), int(m.group(2)), m.group(3) == "1"
     s = {0: 2, 1: 2, 2: 1, 3: 3}[opt]
-    if pull or nw <= 5 * s or not (nw <= 16 or nw in (20, 24, 32)):
+    least = {1: 6, 2: 6, 3: 14}[s]
+    if pull or nw < least or not (nw <= 16 or nw in (20, 24, 32)):
         return 0
     tiles = (40 * 1024) // (s * 4 * 1024)
     return 4 * tiles * s * 4 * 1024
 
 
 def test_stash_rule_covers_the_measured_cases():
-    # momentum / Nesterov with 11-16 workers, plain SGD with 6-16, Adam with
-    # 16; never with pushpull
+    # momentum / Nesterov and plain SGD with 6-16 workers, Adam with 14-16;
+    # never with pushpull
     with_stash = sorted((nw, opt) for nw in range(1, 17) for opt in range(4)
                         if _stash_lds(f"fused_step_fixedILi{nw}ELi{opt}ELb0E"))
-    assert with_stash == sorted([(n, o) for n in range(11, 17) for o in (0, 1)] +
-                                [(n, 2) for n in range(6, 17)] + [(16, 3)])
+    assert with_stash == sorted([(n, o) for n in range(6, 17) for o in (0, 1, 2)] +
+                                [(n, 3) for n in range(14, 17)])
     assert _stash_lds("fused_step_fixedILi16ELi1ELb0E") == 160 * 1024
+    assert _stash_lds("fused_step_fixedILi8ELi1ELb0E") == 160 * 1024
     assert _stash_lds("fused_step_fixedILi8ELi2ELb0E") == 160 * 1024
-    assert _stash_lds("fused_step_fixedILi10ELi1ELb0E") == 0
+    assert _stash_lds("fused_step_fixedILi5ELi1ELb0E") == 0
+    assert _stash_lds("fused_step_fixedILi13ELi3ELb0E") == 0
     assert _stash_lds("fused_step_fixedILi16ELi3ELb0E") == 144 * 1024
     assert _stash_lds("fused_step_fixedILi16ELi1ELb1E") == 0
+
+
+def test_only_burst_kernels_read_the_wall_clock(asm):
+    for name in _kernels(asm):
+        reads = "s_memrealtime" in _body(asm, name)
+        assert reads == bool(_stash_lds(name)), name
 
 
 def test_every_kernel_keeps_its_data_in_registers(asm):

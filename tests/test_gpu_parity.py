@@ -319,18 +319,22 @@ def test_default_cache_budget_is_shared(lib, torch_dev):
         tiny = TorchJob(Job("budget.tiny", 1, (1000,)), dev, lib=lib)
         assert tiny.cached_fraction() == 1.0
         tiny.destroy()
-        # plain SGD with burst write-back (6-16, 20, 24, 32 workers) and every
-        # job with 20, 24 or 32 workers take none of the default budget; the
-        # any-N kernel (17 workers) has no bursts and caches
+        # jobs with burst write-back (momentum and plain SGD with 6-16, 20, 24
+        # or 32 workers, Adam with 14-16, 20, 24 or 32) take none of the
+        # default budget; the others, the any-N kernel (17 workers) and the
+        # unfused variant cache
         for n, opt, want in ((6, "sgd", 0.0), (16, "sgd", 0.0), (5, "sgd", 1.0), (17, "sgd", 1.0),
-                             (16, None, 1.0), (17, None, 1.0), (32, None, 0.0), (20, "adam", 0.0),
-                             (24, "sgd", 0.0)):
+                             (5, None, 1.0), (6, None, 0.0), (8, None, 0.0), (16, None, 0.0),
+                             (17, None, 1.0), (32, None, 0.0), (13, "adam", 1.0), (14, "adam", 0.0),
+                             (20, "adam", 0.0), (24, "sgd", 0.0)):
             jb = TorchJob(Job("budget.n", n, (1000,)), dev, lib=lib, optimizer=opt)
             assert jb.cached_fraction() == want, (n, opt)
             jb.destroy()
-        sgd = TorchJob(Job("budget.sgd", 8, (1000,)), dev, lib=lib, optimizer="sgd", unfused=True)
-        assert sgd.cached_fraction() == 1.0
-        sgd.destroy()
+        for opt in ("sgd", None):
+            jb = TorchJob(Job("budget.unfused", 8, (1000,)), dev, lib=lib, optimizer=opt,
+                          unfused=True)
+            assert jb.cached_fraction() == 1.0, opt
+            jb.destroy()
         # an explicit budget that ends inside the key: cut at a tile boundary
         f = TorchJob(spec, dev, lib=lib, resident_bytes=8 * 5000)
         assert f.info()[4] == 8 * 4096
@@ -457,83 +461,9 @@ def test_concurrent_jobs_equal_sequential(lib, torch_dev):
 
 # --------------------------------------------------------------------------
 # Full-size workloads in the benchmark's launch configuration, checked on
-# sampled elements that the oracle recomputes one by one.
+# every element (tests/test_gpu_fullsize.py).  The largest key below is
+# checked on sampled elements that the oracle recomputes one by one.
 # --------------------------------------------------------------------------
-
-def _sample_positions(spec, rng, n_random=20000):
-    """Element positions (key, index) covering random elements, each key's
-    first and last elements and elements around chunk boundaries."""
-    pos = set()
-    C = spec.chunk_elems
-    for k, n in enumerate(spec.key_elems):
-        for i in list(range(min(n, 3))) + list(range(max(0, n - 5), n)):
-            pos.add((k, i))
-        if n > C:
-            for c in range(C, n, C)[:4]:
-                for i in (c - 1, c, c + 1):
-                    if i < n:
-                        pos.add((k, i))
-    P = spec.num_params
-    flat = rng.integers(0, P, size=n_random)
-    bounds = np.cumsum([0] + list(spec.key_elems))
-    keys = np.searchsorted(bounds, flat, side="right") - 1
-    for k, f in zip(keys, flat):
-        pos.add((int(k), int(f - bounds[k])))
-    return sorted(pos)
-
-
-@pytest.mark.parametrize("name,own_streams", [("resnet50", True), ("alexnet", True),
-                                               ("resnet269", True), ("multitenant", True),
-                                               ("multitenant", False)])
-def test_full_size_workload_sampled(lib, torch_dev, name, own_streams):
-    """As the benchmark runs it: the jobs of a multi-job workload each on
-    their own stream (and, as the option, all on one shared stream)."""
-    torch, dev = torch_dev
-    wl = workloads.workload(name)
-    steps = 2
-    _say("full size", name, "own streams" if own_streams else "", workloads.describe(wl))
-    shared = torch.cuda.Stream(device=dev)
-    jobs, grads, w0s = [], [], []
-    for ji, spec in enumerate(wl.jobs):
-        stream = torch.cuda.Stream(device=dev) if own_streams else shared
-        job = TorchJob(spec, dev, stream=stream, lib=lib)
-        w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
-        job.set_weights(w0)
-        g = [[workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, t, w)
-              for w in range(spec.num_workers)] for t in range(steps)]
-        jobs.append(job)
-        grads.append(g)
-        w0s.append(w0)
-    torch.cuda.synchronize()
-    for t in range(steps):
-        for job, g in zip(jobs, grads):
-            for w, a in enumerate(g[t]):
-                job.attach_grads(w, a)
-            job.push_and_step()
-    for ji, (job, spec) in enumerate(zip(jobs, wl.jobs)):
-        W, M = job.state_arenas()
-        rng = np.random.default_rng(ji)
-        pos = _sample_positions(spec, rng)
-        idx = np.array([job.offsets[k] + i for k, i in pos], dtype=np.int64)
-        tidx = torch.from_numpy(idx).to(dev)
-        gs = [[grads[ji][t][w].index_select(0, tidx).cpu().numpy() for w in range(spec.num_workers)]
-              for t in range(steps)]
-        ws = w0s[ji].index_select(0, tidx).cpu().numpy()
-        ms = np.zeros_like(ws)
-        for t in range(steps):
-            oracle.step_flat(gs[t], ws, ms, spec.lr, spec.momentum, spec.weight_decay, spec.nesterov)
-        _say(f"  {spec.name}: {idx.size} sampled elements; W rel err {_rel_err(W[idx], ws):.3g}")
-        assert _bits_equal(W[idx], ws), f"{spec.name}: W mismatch"
-        assert _bits_equal(M[idx], ms), f"{spec.name}: M mismatch"
-        # untouched arena padding stays zero
-        pad = np.ones(W.size, bool)
-        for o, n in zip(job.offsets, spec.key_elems):
-            pad[o:o + n] = False
-        assert not W[pad].any() and not M[pad].any()
-        job.destroy()
-    del grads
-    torch.cuda.empty_cache()
-
 
 def test_key_past_four_gib_sampled(lib, torch_dev):
     """One key of 1.2 G elements (4.8 GB per array, the largest size here):

@@ -1,9 +1,11 @@
 """GPU parity of the streamed bin's burst write-back (the LDS stash of the
-fixed-N kernels): every worker count and optimizer that has it, with
-grids small enough that a wave walks many tiles (several full write-backs
-and a partial last one), with nothing cached and with a cache budget that
-ends inside a key, in one launch or one per readiness group; bit-exact
-against the CPU oracle over two steps."""
+fixed-N kernels): worker counts and optimizers that have it, with grids
+small enough that a wave walks many tiles (several full write-backs and a
+partial last one), with nothing cached and with a cache budget that ends
+inside a key, in one launch or one per readiness group; bit-exact against
+the CPU oracle over two steps.  The stash is written back when the wall
+clock is in a write window as well as when it is full, so how many tiles a
+write-back covers changes from run to run: the results must not."""
 
 import sys
 
@@ -18,13 +20,14 @@ pytestmark = pytest.mark.gpu
 
 LR, MU, WD, B1, B2, EPS = 0.05, 0.9, 1e-3, 0.9, 0.999, 1e-8
 
-# (workers, optimizer): kernels that stash (N > 5 S: momentum and Nesterov
-# with 11-16 workers, plain SGD with 6-16, Adam with 16), and, next to them,
-# counts at the rule's edge (10 momentum, 5 SGD, 15 Adam) that write piece by
-# piece
-STASHED = [(11, "momentum"), (12, "nesterov"), (13, "momentum"), (14, "nesterov"),
-           (15, "momentum"), (16, "nesterov"), (16, "momentum"), (6, "sgd"), (8, "sgd"),
-           (11, "sgd"), (16, "sgd"), (16, "adam"), (10, "momentum"), (5, "sgd"), (15, "adam")]
+# (workers, optimizer): kernels that stash (momentum, Nesterov and plain SGD
+# with 6-16 workers, Adam with 14-16), and, next to them, counts at the
+# rule's edge (5 momentum, 5 SGD, 13 Adam) that write piece by piece
+STASHED = [(6, "nesterov"), (7, "momentum"), (8, "nesterov"), (8, "momentum"), (9, "nesterov"),
+           (10, "momentum"), (11, "momentum"), (12, "nesterov"), (13, "momentum"),
+           (14, "nesterov"), (15, "momentum"), (16, "nesterov"), (16, "momentum"), (6, "sgd"),
+           (8, "sgd"), (11, "sgd"), (16, "sgd"), (14, "adam"), (15, "adam"), (16, "adam"),
+           (5, "momentum"), (5, "sgd"), (13, "adam")]
 # 107 full tiles and ragged ends: a wave of a 1-workgroup grid (4 waves)
 # walks about 27 tiles
 KEYS = (5, 1024 * 37 + 3, 70001, 1024 * 11, 4097, 1, 1024 * 6)
@@ -116,8 +119,8 @@ def test_burst_write_back_matches_the_oracle(lib, torch_dev, n, opt, workgroups,
     _run(lib, torch_dev, n, opt, workgroups, resident)
 
 
-@pytest.mark.parametrize("n,opt", [(16, "nesterov"), (13, "momentum"), (11, "sgd"), (24, "momentum"),
-                                   (32, "sgd"), (20, "adam")])
+@pytest.mark.parametrize("n,opt", [(16, "nesterov"), (13, "momentum"), (8, "nesterov"), (11, "sgd"),
+                                   (24, "momentum"), (32, "sgd"), (20, "adam"), (14, "adam")])
 @pytest.mark.parametrize("workgroups,resident", [(1, 0), (None, "partial")])
 def test_burst_write_back_per_readiness_group(lib, torch_dev, n, opt, workgroups, resident):
     """Each readiness group's launch walks its own tiles: the stash is
