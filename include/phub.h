@@ -351,6 +351,44 @@ int phub_job_info(phub_job *job, int *workgroups, int *threads_per_group, int64_
  */
 int phub_destroy(phub_job *job);
 
+/*
+ * phub_step_noalloc - one exchange step that allocates no memory: for
+ * callers that cannot allocate device memory (serving loops that must not
+ * call hipMalloc, harnesses that forbid allocation).  It computes what
+ * phub_init + phub_push_all + phub_step compute for one step of a momentum
+ * job created with the same arguments, on caller-owned state.
+ *   num_workers, num_keys, key_elems, chunk_bytes, lr, momentum,
+ *   weight_decay, nesterov
+ *                 as phub_init (same limits).
+ *   grads         host array of num_workers * num_keys device pointers,
+ *                 grads[w * num_keys + k] worker w's gradient for key k (as
+ *                 phub_push_all); read during the call only.
+ *   weights, moments
+ *                 device arenas of W and M (fp32, 16-byte aligned), updated
+ *                 in place, laid out like a job's state: key k starts at
+ *                 element A_k = sum over j < k of n_j rounded up to a
+ *                 multiple of 64; the padding is neither read nor written.
+ *                 NULL only when every key is empty.
+ *   hip_stream    the hipStream_t the step is ordered on (NULL = the null
+ *                 stream).
+ * The step's schedule and pointer table live in a device array of the
+ * library of 4 MiB (PHUB_NOALLOC_SCRATCH_BYTES), one per GPU, held until
+ * the process ends; that bounds a call to about 250 M parameters and
+ * PHUB_EINVAL reports a step that does not fit, before anything is
+ * enqueued.  The call uploads the schedule on hip_stream after the stream's
+ * earlier work and waits for that upload (the host thread blocks until the
+ * stream's earlier work is done); the kernel itself runs asynchronously.
+ * Calls on one GPU share its array: calls that overlap on one GPU (from
+ * other threads, or on another stream before this call's kernel has run)
+ * race and give wrong results.  All state streams non-temporally (nothing
+ * is kept in the memory-side cache).  Errors: PHUB_EINVAL, PHUB_ENOMEM (host
+ * memory), PHUB_EHIP.
+ */
+int phub_step_noalloc(int num_workers, int num_keys, const int64_t *key_elems,
+                      int64_t chunk_bytes, float lr, float momentum, float weight_decay,
+                      int nesterov, const float *const *grads, float *weights, float *moments,
+                      void *hip_stream);
+
 /* Message of the last failed call on this thread ("" if none).  The string
  * belongs to the library and lives until the thread's next failing call. */
 const char *phub_last_error(void);

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libphub.so")
 PROBE_LIB = os.path.join(PKG, "libphub_probe.so")
 PROBE_SOURCES = ["probe.hip"]
 
-SOURCES = ["plan.cpp", "phub_api.cpp", "fused_step.hip"]
+SOURCES = ["plan.cpp", "phub_api.cpp", "fused_step.hip", "step_noalloc.hip"]
 HEADERS = ["plan.hpp", "kernels.hpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

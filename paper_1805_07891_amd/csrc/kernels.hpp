@@ -3,7 +3,12 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cstdint>
+#include <string>
+#include <vector>
+
+#include "plan.hpp"
 
 namespace phub {
 
@@ -87,6 +92,18 @@ constexpr bool burst_write_back(int num_workers, int num_states) {
 constexpr int64_t kWritePeriodNsPerStream = 3200;
 constexpr int64_t kWriteWindowNs = 15360;
 
+// Write-phase period and window of the burst write-back in ticks of a wall
+// clock running at clock_khz, for a job with num_workers gradients and
+// num_states state arrays.
+inline void write_phase_ticks(int num_workers, int num_states, int64_t clock_khz,
+                              uint32_t* period, uint32_t* window) {
+    const int64_t streams = num_workers + 2 * int64_t(num_states);
+    const int64_t p = kWritePeriodNsPerStream * streams * clock_khz / 1000000;
+    const int64_t w = kWriteWindowNs * clock_khz / 1000000;
+    *period = uint32_t(std::min<int64_t>(std::max<int64_t>(p, 2), INT32_MAX));
+    *window = uint32_t(std::min<int64_t>(std::max<int64_t>(w, 1), *period - 1));
+}
+
 // Scalars of one launch.  For Adam, c1 = 1 - b1, c2 = 1 - b2 and the
 // step's bias corrections k1 = lr / (1 - b1^t), k2 = 1 / (1 - b2^t) are
 // computed on the host in double and rounded to fp32 once.
@@ -122,6 +139,38 @@ struct StepParams {
     OptArgs opt;
     int num_workers;
 };
+
+// A part of a key scheduled on its own (a job's cache-resident or
+// streamed part of the key): the key's row in the gradient pointer table,
+// the part's first element within the key (a multiple of 4) and its
+// element count.
+struct VirtualKey {
+    int row;
+    int64_t base;
+    int64_t elems;
+};
+
+// Device form of schedules: full tiles and remainders grouped by bin, and
+// offsets into them (each bin ends where the next begins).
+struct DeviceTables {
+    std::vector<DevTile> tiles;
+    std::vector<DevRem> rems;
+    std::vector<int32_t> tile_begin;
+    std::vector<int32_t> rem_begin;
+};
+
+// Appends the device form of `plan` (built over `vkeys`) to `out`: for each
+// of its first `bins` bins, the bin's segments in order, each cut into its
+// full tiles and at most one remainder, then the end offsets of the bin.
+// row_arena_offset[row] is the arena element offset of the key on that
+// row.  Returns the number of elements scheduled, or -1 (nothing usable
+// appended) when a table outgrows 32-bit offsets.
+int64_t append_device_tables(const Plan& plan, const std::vector<VirtualKey>& vkeys,
+                             const std::vector<int64_t>& row_arena_offset, int bins,
+                             DeviceTables* out);
+
+// Sets the calling thread's error message (phub_last_error) and returns code.
+int report_error(int code, const std::string& message);
 
 // Enqueues one fused aggregate + optimize pass over the whole schedule
 // (and, when p.outs is set, writes the updated weights into every worker's

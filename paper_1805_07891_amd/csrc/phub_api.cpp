@@ -293,12 +293,8 @@ phub::OptArgs optimizer_args(const phub_job* j) {
     o.nlr = -j->lr;
     o.mu = j->mu;
     o.wd = j->wd;
-    // write phases of the burst write-back, in wall-clock ticks
-    const int64_t streams = j->num_workers + 2 * int64_t(j->num_states);
-    const int64_t period = phub::kWritePeriodNsPerStream * streams * j->wall_clock_khz / 1000000;
-    const int64_t window = phub::kWriteWindowNs * j->wall_clock_khz / 1000000;
-    o.wb_period = uint32_t(std::min<int64_t>(std::max<int64_t>(period, 2), INT32_MAX));
-    o.wb_window = uint32_t(std::min<int64_t>(std::max<int64_t>(window, 1), o.wb_period - 1));
+    phub::write_phase_ticks(j->num_workers, j->num_states, j->wall_clock_khz, &o.wb_period,
+                            &o.wb_window);
     if (j->opt == phub::kOptAdam) {
         const double t = double(j->steps_done + 1);
         o.b1 = j->b1;
@@ -425,6 +421,42 @@ int record_push(phub_job* j, int worker, int key, const float* grad, hipEvent_t 
 }
 
 }  // namespace
+
+namespace phub {
+
+int report_error(int code, const std::string& message) {
+    g_error = message;
+    return code;
+}
+
+int64_t append_device_tables(const Plan& plan, const std::vector<VirtualKey>& vkeys,
+                             const std::vector<int64_t>& row_arena_offset, int bins,
+                             DeviceTables* out) {
+    int64_t elems = 0;
+    for (int b = 0; b < bins; ++b) {
+        for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
+            const PlanSegment& sg = plan.segments[i];
+            const VirtualKey& v = vkeys[sg.key];
+            const int64_t koff = v.base + sg.offset;  // first element within the key
+            const int64_t ao = row_arena_offset[v.row] + koff;
+            elems += sg.count;
+            const int64_t nfull = sg.count / kTileElems;
+            for (int64_t t = 0; t < nfull; ++t)
+                out->tiles.push_back(
+                    {ao + t * kTileElems, v.row, uint32_t((koff + t * kTileElems) / 4)});
+            const int64_t done = nfull * kTileElems;
+            if (done < sg.count)
+                out->rems.push_back({ao + done, koff + done, v.row, int32_t(sg.count - done), 0});
+        }
+        if (out->tiles.size() > size_t(INT32_MAX) || out->rems.size() > size_t(INT32_MAX))
+            return -1;
+        out->tile_begin.push_back(int32_t(out->tiles.size()));
+        out->rem_begin.push_back(int32_t(out->rems.size()));
+    }
+    return elems;
+}
+
+}  // namespace phub
 
 extern "C" {
 
@@ -658,11 +690,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     // key (the part below the cut is resident), so both parts keep the
     // 16-byte alignment of the key's start.  A part is a "virtual key": a
     // row and a first element within the key.
-    struct VKey {
-        int row;
-        int64_t base;
-        int64_t elems;
-    };
+    using VKey = phub::VirtualKey;
     std::vector<phub::Plan> plans;  // [group * 2 + phase]
     std::vector<std::vector<VKey>> vkeys;
     {
@@ -763,40 +791,28 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         // 2 * bins + 1 offsets per readiness group (the resident bins, then
         // the streamed ones).  A descriptor's key is the key's row in the
         // pointer table.
-        std::vector<phub::DevTile> dtiles;
-        std::vector<phub::DevRem> drems;
-        std::vector<int32_t> tile_begin, rem_begin;
-        for (int g = 0; g < j->num_rgroups; ++g) {
-            tile_begin.push_back(int32_t(dtiles.size()));
-            rem_begin.push_back(int32_t(drems.size()));
-            for (int ph = 0; ph < 2; ++ph) {
-                const phub::Plan& plan = plans[g * 2 + ph];
-                const std::vector<VKey>& vk = vkeys[g * 2 + ph];
-                for (int b = 0; b < j->bins; ++b) {
-                    for (int64_t i = plan.bin_begin[b]; i < plan.bin_begin[b + 1]; ++i) {
-                        const phub::PlanSegment& sg = plan.segments[i];
-                        const VKey& v = vk[sg.key];
-                        const int64_t koff = v.base + sg.offset;  // first element within the key
-                        const int64_t ao = j->arena_offset[j->key_of_row[v.row]] + koff;
-                        if (ph == 0) j->resident_bytes += int64_t(sg.count) * elem_state_bytes;
-                        const int64_t nfull = sg.count / phub::kTileElems;
-                        for (int64_t t = 0; t < nfull; ++t)
-                            dtiles.push_back({ao + t * phub::kTileElems, v.row,
-                                              uint32_t((koff + t * phub::kTileElems) / 4)});
-                        const int64_t done = nfull * phub::kTileElems;
-                        if (done < sg.count)
-                            drems.push_back({ao + done, koff + done, v.row,
-                                             int32_t(sg.count - done), 0});
-                    }
-                    if (dtiles.size() > size_t(INT32_MAX) || drems.size() > size_t(INT32_MAX)) {
+        phub::DeviceTables dt;
+        {
+            std::vector<int64_t> row_arena_offset(num_keys);
+            for (int r = 0; r < num_keys; ++r) row_arena_offset[r] = j->arena_offset[j->key_of_row[r]];
+            for (int g = 0; g < j->num_rgroups; ++g) {
+                dt.tile_begin.push_back(int32_t(dt.tiles.size()));
+                dt.rem_begin.push_back(int32_t(dt.rems.size()));
+                for (int ph = 0; ph < 2; ++ph) {
+                    const int64_t elems = phub::append_device_tables(
+                        plans[g * 2 + ph], vkeys[g * 2 + ph], row_arena_offset, j->bins, &dt);
+                    if (elems < 0) {
                         rc = fail(PHUB_EINVAL, "schedule too large");
                         goto fail_cleanup;
                     }
-                    tile_begin.push_back(int32_t(dtiles.size()));
-                    rem_begin.push_back(int32_t(drems.size()));
+                    if (ph == 0) j->resident_bytes += elems * elem_state_bytes;
                 }
             }
         }
+        const std::vector<phub::DevTile>& dtiles = dt.tiles;
+        const std::vector<phub::DevRem>& drems = dt.rems;
+        const std::vector<int32_t>& tile_begin = dt.tile_begin;
+        const std::vector<int32_t>& rem_begin = dt.rem_begin;
         j->num_tiles = int64_t(dtiles.size());
         j->num_rems = int64_t(drems.size());
         const size_t tile_bytes = std::max<size_t>(dtiles.size(), 1) * sizeof(phub::DevTile);

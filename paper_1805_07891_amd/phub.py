@@ -42,7 +42,7 @@ EXPORTED = ("phub_init", "phub_init_ex", "phub_set_weights", "phub_push", "phub_
             "phub_step", "phub_pull", "phub_get_state", "phub_get_second_moment", "phub_sync",
             "phub_get_stream",
             "phub_job_info", "phub_destroy", "phub_last_error", "phub_plan_count",
-            "phub_plan_build")
+            "phub_plan_build", "phub_step_noalloc")
 
 
 class PhubError(RuntimeError):
@@ -98,6 +98,7 @@ class Library:
             "phub_plan_count": ([i32, i32, vp, i64, i32, i32, i32, ctypes.POINTER(i64),
                                  ctypes.POINTER(i32), ctypes.POINTER(i64)], i32),
             "phub_plan_build": ([i32, i32, vp, i64, i32, i32, i32, vp, vp, vp], i32),
+            "phub_step_noalloc": ([i32, i32, vp, i64, f32, f32, f32, i32, vp, vp, vp, vp], i32),
         }
         for name, (args, res) in sig.items():
             fn = getattr(lib, name)
@@ -253,6 +254,18 @@ class Library:
 
     def phub_destroy(self, job, check: bool = True) -> int:
         return self._check(self.lib.phub_destroy(job), check)
+
+    def phub_step_noalloc(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,
+                          lr: float, momentum: float, weight_decay: float, nesterov: bool,
+                          grad_ptrs: Sequence[int], weights_ptr: int, moments_ptr: int,
+                          stream: Optional[int] = None, check: bool = True) -> int:
+        """One step without allocation over caller arenas (see phub.h);
+        grad_ptrs[w * K + k] is worker w's gradient for key k."""
+        elems = (ctypes.c_int64 * len(key_elems))(*[int(n) for n in key_elems])
+        return self._check(self.lib.phub_step_noalloc(
+            int(num_workers), len(key_elems), elems, int(chunk_bytes), float(lr), float(momentum),
+            float(weight_decay), int(bool(nesterov)), pointer_array(grad_ptrs), weights_ptr,
+            moments_ptr, stream), check)
 
     # -- schedule (host only) ----------------------------------------------
     def phub_plan_count(self, num_workers: int, key_elems: Sequence[int], chunk_bytes: int,

@@ -272,3 +272,27 @@ def test_calls_on_a_dead_handle_return_estate(lib):
                lambda: lib.phub_destroy(None, check=False)):
         assert fn() == phub.PHUB_ESTATE
     assert "live job" in lib.last_error()
+
+
+def test_noalloc_step_rejects_bad_arguments_before_touching_the_gpu(lib):
+    """Every argument error of phub_step_noalloc, including a step whose
+    schedule would not fit the library's scratch array, is found on the host
+    before any HIP call (there is no GPU here): the pointers below are never
+    dereferenced."""
+    fake = 1 << 20  # a 16-byte aligned address that is never used
+    for kw in [dict(num_workers=0), dict(chunk_bytes=20), dict(lr=float("nan")),
+               dict(weight_decay=float("inf")), dict(key_elems=[4, 1 << 34]),
+               dict(grads=[0, fake, fake, fake]), dict(grads=[fake + 4, fake, fake, fake]),
+               dict(weights=0), dict(moments=fake + 8),
+               dict(key_elems=[300 << 20, 4]),              # about 4.7 MB of tiles
+               dict(num_workers=2, key_elems=[1] * 300000,  # 4.8 MB of gradient pointers
+                    grads=[fake] * 600000)]:
+        a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
+                 weight_decay=1e-4, nesterov=True, grads=[fake] * 4, weights=fake,
+                 moments=fake)
+        a.update(kw)
+        rc = lib.phub_step_noalloc(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["lr"],
+                                   a["momentum"], a["weight_decay"], a["nesterov"], a["grads"],
+                                   a["weights"], a["moments"], check=False)
+        assert rc == phub.PHUB_EINVAL, (kw.keys(), rc, lib.last_error())
+    assert "scratch" in lib.last_error()
