@@ -3,15 +3,20 @@
 
 One step = every worker pushes all its keys (pointer registration) and the
 job runs one fused aggregate + optimize launch over all keys, for every job
-of the workload.  Gradients, weights and momentum are resident in HBM before
-the timed region starts.  Prints one JSON line:
+of the workload (the tenants of a multi-job workload each on their own
+stream, concurrently).  Gradients, weights and momentum are resident in HBM
+before the timed region starts.  Prints one JSON line:
 
   metric   worker-gradient GB/s aggregated+optimized per step
   value    N * P * 4 bytes per step / wall time per step, summed over jobs
   roofline the fused kernel's algorithmic HBM bytes ((N + 4) * P * 4 per
-           launch) / its average launch duration, measured with HIP events on
-           the job's stream, against the 8 TB/s HBM3E peak
+           launch, summed over the step's launches) / its duration, measured
+           with HIP events on the jobs' streams, against the 8 TB/s HBM3E
+           peak, beside ceilings measured in the same run (read-only,
+           write-only and mixed read/write streams)
   cpu_baseline the CPU oracle timed on the host over a bounded sample
+  configs  (without --workload) the same figures, compact, for each of the
+           five workloads; the top-level line is the multi-tenant workload
 
 Usage: python bench.py [--steps K] [--warmup W] [--workload NAME]
 """
@@ -34,7 +39,7 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCES = ["paper_1805_07891_amd/csrc/fused_step.hip", "paper_1805_07891_amd/csrc/kernels.hpp",
                   "paper_1805_07891_amd/csrc/plan.cpp", "paper_1805_07891_amd/csrc/plan.hpp",
                   "paper_1805_07891_amd/csrc/phub_api.cpp"]
-DEFAULT_WORKLOAD = "resnet50"
+HEADLINE_WORKLOAD = "multitenant"
 
 
 def _code_only(text: str) -> str:
@@ -69,8 +74,9 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per launch from the committed counter summary, if it was
-    taken on the kernel as it is now (same source hash); else None."""
+    """HBM bytes per step (all of the step's launches) from the committed
+    counter summary, if it was taken on the kernel as it is now (same source
+    hash); else None."""
     path = os.path.join(ROOT, "profiles", f"fused_step_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -78,7 +84,7 @@ def measured_traffic(workload: str):
         rec = json.load(f)
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("bytes_per_step")
 
 
 NOTES = {
@@ -87,38 +93,78 @@ NOTES = {
 }
 
 
-def read_ceiling(torch, dev, arenas, reps: int = 5):
-    """Measured HBM read ceiling of the same buffers in the same run: the
-    bandwidth probe (a read-only non-temporal stream, no arithmetic) over the
-    dominant job's gradient arenas; best of `reps` passes."""
+def _probe_lib():
     import ctypes
     from paper_1805_07891_amd import build as hip_build
     if not os.path.exists(hip_build.PROBE_LIB):
         raise RuntimeError(f"{hip_build.PROBE_LIB} is not built; run __graft_entry__.build()")
     lib = ctypes.CDLL(hip_build.PROBE_LIB)
-    lib.phub_probe_read.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_int64,
-                                    ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
-    lib.phub_probe_read.restype = ctypes.c_int
+    vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    lib.phub_probe_read.argtypes = [pp, i32, i64, i32, f32, vp, vp]
+    lib.phub_probe_write.argtypes = [pp, i32, i64, i32, f32, vp]
+    lib.phub_probe_mixed.argtypes = [pp, i32, pp, i32, i64, i32, f32, vp, vp]
+    for f in (lib.phub_probe_read, lib.phub_probe_write, lib.phub_probe_mixed):
+        f.restype = i32
+    lib.phub_probe_tile_elems.restype = i32
+    return lib
+
+
+def ceilings(torch, dev, grads, num_states: int, stream, reps: int = 5):
+    """HBM ceilings measured in the same run over the dominant job's buffers
+    (best of `reps` passes each, GB/s): the bandwidth probes reading its N
+    gradient arenas (read-only), writing S scratch arenas of the same size
+    (write-only), and reading the N arenas while reading and writing back
+    the S scratch arenas in place, tile by tile (the step's (N + S) : S mix of
+    reads and writes without its arithmetic or the timing of its writes).
+    Also the phase-separated bound: the step's bytes if its reads ran at the
+    read ceiling and its writes at the write ceiling, one after the other."""
+    import ctypes
+    lib = _probe_lib()
     tile = lib.phub_probe_tile_elems()
-    n = min(a.numel() for a in arenas) // tile * tile
-    ptrs = (ctypes.c_void_p * len(arenas))(*[a.data_ptr() for a in arenas])
+    n = min(a.numel() for a in grads) // tile * tile
+    scratch = [torch.zeros(n, dtype=torch.float32, device=dev) for _ in range(num_states)]
     grid = torch.cuda.get_device_properties(dev).multi_processor_count
     sink = torch.empty(grid * 256, dtype=torch.float32, device=dev)
-    stream = torch.cuda.Stream(device=dev)
-    best = 0.0
-    for _ in range(reps + 1):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        rc = lib.phub_probe_read(ptrs, len(arenas), n, grid, -1.2345678e30, ctypes.c_void_p(sink.data_ptr()),
-                                 ctypes.c_void_p(stream.cuda_stream))
-        e1.record(stream)
-        if rc != 0:
-            raise RuntimeError(f"phub_probe_read failed: {rc}")
-        torch.cuda.synchronize()
-        best = max(best, len(arenas) * n * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9)
-    return {"GBps": round(best, 1), "frac_of_peak": round(best / HBM_PEAK_GBS, 4),
-            "kind": "read-only non-temporal stream over the dominant job's gradient arenas",
-            "bytes": len(arenas) * n * 4}
+    gp = (ctypes.c_void_p * len(grads))(*[a.data_ptr() for a in grads])
+    sp = (ctypes.c_void_p * num_states)(*[a.data_ptr() for a in scratch])
+    sv = ctypes.c_void_p(stream.cuda_stream)
+    sk = ctypes.c_void_p(sink.data_ptr())
+    runs = {
+        "read": (lambda: lib.phub_probe_read(gp, len(grads), n, grid, -1.2345678e30, sk, sv),
+                 len(grads) * n * 4),
+        "write": (lambda: lib.phub_probe_write(sp, num_states, n, grid, 0.0, sv),
+                  num_states * n * 4),
+        "mixed": (lambda: lib.phub_probe_mixed(gp, len(grads), sp, num_states, n, grid,
+                                               -1.2345678e30, sk, sv),
+                  (len(grads) + 2 * num_states) * n * 4),
+    }
+    torch.cuda.synchronize()
+    best = {}
+    for name, (run, nbytes) in runs.items():
+        b = 0.0
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = run()
+            e1.record(stream)
+            if rc != 0:
+                raise RuntimeError(f"phub_probe_{name} failed: {rc}")
+            torch.cuda.synchronize()
+            b = max(b, nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+        best[name] = b
+    del scratch
+    nr, nw = len(grads) + num_states, num_states
+    phase = (nr + nw) / (nr / best["read"] + nw / best["write"])
+    out = {k: {"GBps": round(v, 1), "frac_of_peak": round(v / HBM_PEAK_GBS, 4)} for k, v in best.items()}
+    out["read"]["kind"] = "read-only non-temporal stream over the dominant job's gradient arenas"
+    out["write"]["kind"] = f"write-only non-temporal stream over {num_states} arenas of the same size"
+    out["mixed"]["kind"] = (f"the {len(grads)} gradient arenas read and {num_states} arenas read and "
+                            f"written back in place, tile by tile ({nr}:{nw} reads:writes)")
+    out["phase_separated"] = {"GBps": round(phase, 1), "frac_of_peak": round(phase / HBM_PEAK_GBS, 4),
+                              "kind": "the step's reads at the read ceiling, then its writes at the "
+                                      "write ceiling"}
+    return out
 
 
 def cu_masked_streams(torch, dev, wl):
@@ -149,37 +195,78 @@ def cu_masked_streams(torch, dev, wl):
     return out
 
 
-def cold_launches(torch, dev, jobs, dom, push, steps: int, dom_bytes: int):
-    """The dominant job's kernel with a cold memory-side cache: before each
-    job's step, a 1 GiB buffer is read with ordinary (cache-allocating)
-    loads on that job's stream, which replaces the 256 MiB cache's contents
-    with clean lines, so that cache-resident state starts from HBM (and no
-    dirty data of the flush is written back during the step).  Only the
-    step is timed (HIP events on the job's stream)."""
+def span_of_steps(torch, dev, jobs, push, steps: int, helper, before=None):
+    """Device time of one step of every job (ms; a list).  Without `before`:
+    `steps` steps back to back between one pair of HIP events, on the job's
+    stream for one job, else on a helper stream that every job stream waits
+    on at the start and that waits on every job stream at the end (the
+    tenants' launches overlap); one value, the average.  With `before`
+    (e.g. a cache flush), called on each job's stream before each step,
+    every step is timed on its own after its `before` work has completed;
+    one value per step.  `helper` is a stream of its own (unused for one
+    job)."""
+    one = len(jobs) == 1
+    if one:
+        helper = jobs[0].stream
+    ms = []
+    for _ in range(steps if before is not None else 1):
+        if before is not None:
+            for job in jobs:
+                with torch.cuda.stream(job.stream):
+                    before()
+                if not one:
+                    done = torch.cuda.Event()
+                    done.record(job.stream)
+                    helper.wait_event(done)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(helper)
+        if not one:
+            for job in jobs:
+                job.stream.wait_event(e0)
+        for _ in range(1 if before is not None else steps):
+            for job in jobs:
+                push(job)
+                job.step()
+        if not one:
+            for job in jobs:
+                ev = torch.cuda.Event()
+                ev.record(job.stream)
+                helper.wait_event(ev)
+        e1.record(helper)
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1) / (1 if before is not None else steps))
+    return ms
+
+
+def cold_steps(torch, dev, jobs, push, steps: int, step_bytes: int, helper):
+    """The step with a cold memory-side cache: before each step, a 1 GiB
+    buffer is read with ordinary (cache-allocating) loads on every job's
+    stream, which replaces the 256 MiB cache's contents with clean lines, so
+    that state cached by the previous step starts from HBM (and no dirty
+    data of the flush is written back during the step).  Each step is timed
+    on its own (span_of_steps), and so are as many steps after a read of a
+    1-element buffer instead (isolated but warm), since an isolated step of
+    concurrent tenants also loses the overlap of one step's tail with the
+    next step's launches."""
     if steps <= 0:
         return None
     flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    tiny = torch.ones(1, dtype=torch.float32, device=dev)
     sink = torch.empty((), dtype=torch.float32, device=dev)
-    durs = []
-    for _ in range(steps):
-        for j, job in enumerate(jobs):
-            with torch.cuda.stream(job.stream):
-                torch.sum(flush, 0, out=sink)
-            push(job)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(job.stream)
-            job.step()
-            e1.record(job.stream)
-            if j == dom:
-                durs.append((e0, e1))
-    torch.cuda.synchronize()
-    ms = sorted(a.elapsed_time(b) for a, b in durs)
-    avg = sum(ms) / len(ms)
+    cold = sorted(span_of_steps(torch, dev, jobs, push, steps, helper,
+                                before=lambda: torch.sum(flush, 0, out=sink)))
+    warm = sorted(span_of_steps(torch, dev, jobs, push, steps, helper,
+                                before=lambda: torch.sum(tiny, 0, out=sink)))
+    avg = sum(cold) / len(cold)
+    wavg = sum(warm) / len(warm)
     del flush
-    return {"kind": "memory-side cache flushed (1 GiB read) before each step",
-            "steps": steps, "avg_launch_us": round(avg * 1e3, 2),
-            "median_launch_us": round(ms[len(ms) // 2] * 1e3, 2),
-            "frac": round(dom_bytes / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    return {"kind": "memory-side cache flushed (1 GiB read) before each step, each step timed "
+                    "on its own",
+            "steps": steps, "avg_step_us": round(avg * 1e3, 2),
+            "median_step_us": round(cold[len(cold) // 2] * 1e3, 2),
+            "frac": round(step_bytes / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "isolated_warm_avg_step_us": round(wavg * 1e3, 2),
+            "isolated_warm_frac": round(step_bytes / (wavg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
 
 
 def cpu_baseline(wl, grads_dev, w0_dev, budget_s: float):
@@ -455,9 +542,13 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--workload", default=None,
+                    help="one workload (tiny, resnet50, alexnet, resnet269, multitenant); "
+                         "default: all five, the multi-tenant one as the headline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="budget of the CPU oracle baseline (0 skips it)")
+                    help="budget of the CPU oracle baseline of the headline workload (0 skips it)")
+    ap.add_argument("--config-cpu-seconds", type=float, default=2.0,
+                    help="budget of the CPU oracle baseline of each other workload (0 skips it)")
     ap.add_argument("--chunk-bytes", type=int, default=None,
                     help="chunk size of the schedule (default: the workload's, 32 KB)")
     ap.add_argument("--schedule", choices=("lpt", "split"), default="lpt",
@@ -529,20 +620,22 @@ def main(argv=None) -> int:
               f"supported.", file=sys.stderr)
         return 2
 
+    if not args.workload and not args.streaming:
+        return run_all(args, argv if argv is not None else sys.argv[1:])
+
     import torch
     from paper_1805_07891_amd import workloads
-    from paper_1805_07891_amd.job import TorchJob, load_library
-    from paper_1805_07891_amd.phub import PHUB_SCHEDULE_SPLIT
+    from paper_1805_07891_amd.job import load_library
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     dev = torch.device("cuda:0")
     lib = load_library()
-    wl = workloads.workload(args.workload)
 
     if args.streaming:
-        return streaming_bench(torch, dev, lib, wl, args)
+        return streaming_bench(torch, dev, lib, workloads.workload(args.workload or "resnet50"),
+                               args)
 
     if args.copy_calibration:
         src = torch.ones(128 << 20, dtype=torch.float32, device=dev)
@@ -552,15 +645,104 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         del src, dst
 
+    wl = workloads.workload(args.workload)
+    # The streams, created first: one per job, then a helper for timing
+    # events and probes.
+    streams = [torch.cuda.Stream(device=dev) for _ in wl.jobs]
+    helper = torch.cuda.Stream(device=dev)
+    line = measure(torch, dev, lib, wl, args, args.cpu_seconds, streams, helper)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+# Flags main() handles itself and does not pass on to a workload's process.
+_OWN_FLAGS = {"--workload": 1, "--cpu-seconds": 1, "--config-cpu-seconds": 1}
+
+
+def run_all(args, argv) -> int:
+    """The five workloads, each measured by this script in a process of its
+    own (this process never touches the GPU).  Measured in one process one
+    after another, every workload after the first lost 1.5-3 points (the
+    multi-tenant step 77.4% -> 75.9% -> 75.2% on three runs in a row,
+    ResNet-269 81.5% -> 79.0% after the multi-tenant run), whatever the
+    order: memory freed by one workload and allocated by the next is laid
+    out differently.  A job of a training run starts in a fresh process, so
+    each workload is measured in one.  The line printed is the headline
+    (multi-tenant) workload's, with every workload's compact figures under
+    "configs"."""
+    import subprocess
+    from paper_1805_07891_amd import workloads
+    passed = []
+    i = 0
+    while i < len(argv):
+        a = argv[i]
+        flag = a.split("=", 1)[0]
+        if flag in _OWN_FLAGS:
+            i += 1 if "=" in a else 1 + _OWN_FLAGS[flag]
+            continue
+        passed.append(a)
+        i += 1
+    lines = {}
+    for name in workloads.WORKLOAD_NAMES:
+        budget = args.cpu_seconds if name == HEADLINE_WORKLOAD else args.config_cpu_seconds
+        cmd = [sys.executable, "-u", os.path.abspath(__file__), "--workload", name,
+               "--cpu-seconds", str(budget), *passed]
+        print(f"bench: {name}", file=sys.stderr, flush=True)
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+        if r.returncode != 0:
+            print(f"bench: {name} failed with status {r.returncode}", file=sys.stderr, flush=True)
+            return r.returncode
+        lines[name] = json.loads(r.stdout.strip().splitlines()[-1])
+    out = lines[HEADLINE_WORKLOAD]
+    out["configs"] = {n: compact(lines[n]) for n in workloads.WORKLOAD_NAMES}
+    out["configs_kind"] = "each workload measured by bench.py --workload NAME in a process of its own"
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def compact(line: dict) -> dict:
+    """The figures of one workload's line that the five-workload summary
+    keeps."""
+    r, c = line["roofline"], line["config"]
+    cold, ceil, base = r.get("cold"), r["ceilings"], line.get("cpu_baseline")
+    step_bytes = r["algorithmic_bytes_per_launch"]
+    return {
+        "ms_per_step": line["ms_per_step"],
+        "value_GBps": line["value"],
+        "whole_step_pct": c["hbm_pct_of_peak_whole_step"],
+        "kernel_frac": r["frac"],
+        "kernel_frac_cold": cold["frac"] if cold else None,
+        "kernel_frac_isolated_warm": cold["isolated_warm_frac"] if cold else None,
+        "state_cached_fraction": [j["state_cached_fraction"] for j in c["jobs"]],
+        "read_ceiling_frac": ceil["read"]["frac_of_peak"],
+        "mixed_ceiling_frac": ceil["mixed"]["frac_of_peak"],
+        "phase_separated_frac": ceil["phase_separated"]["frac_of_peak"],
+        "frac_of_mixed_ceiling": r["frac_of_mixed_ceiling"],
+        "traffic_over_algorithmic": (round(r["traffic"] / step_bytes, 4) if r["traffic"] else None),
+        "host_us_per_step": c["host_us_per_step"],
+        "cpu_baseline_GBps": base["value"] if base else None,
+        "cpu_sample": base["sample"] if base else None,
+    }
+
+
+def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> dict:
+    """One workload: set-up, warm-up, the timed steps, kernel timing,
+    ceilings, cold-cache steps and the CPU baseline.  Job j runs on
+    streams[j] (all on streams[0] with --shared-stream); `helper` carries
+    the timing events of several jobs and the probes.  Returns the JSON
+    line."""
+    from paper_1805_07891_amd import workloads
+    from paper_1805_07891_amd.job import TorchJob
+    from paper_1805_07891_amd.phub import PHUB_SCHEDULE_SPLIT
+
     # Co-running jobs each have their own stream (their launches run
     # concurrently); with --shared-stream they take turns on one stream,
     # each launch with the whole GPU.
     shared_stream = len(wl.jobs) > 1 and args.shared_stream
-    one_stream = torch.cuda.Stream(device=dev)
     masked = cu_masked_streams(torch, dev, wl) if args.cu_masks and len(wl.jobs) > 1 else None
     jobs, grads, w0s = [], [], []
     for ji, spec in enumerate(wl.jobs):
-        stream = one_stream if shared_stream or ji == 0 else torch.cuda.Stream(device=dev)
+        stream = streams[0] if shared_stream else streams[ji]
         if masked is not None:
             stream = masked[ji][0]
         job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
@@ -610,9 +792,10 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
-    # Kernel durations: K more steps with HIP events recorded on each job's
-    # stream around its phub_step (kept out of the wall-clock loop above,
-    # where the event records would add their own time to small steps).
+    # Each job's launches: K more steps with HIP events recorded on each
+    # job's stream around its phub_step (kept out of the wall-clock loop
+    # above, where the event records would add their own time to small
+    # steps).
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(K)] for _ in jobs]
     for s in range(K):
@@ -634,57 +817,50 @@ def main(argv=None) -> int:
     ms_per_step = (t1 - t0) * 1e3 / K
     worker_bytes = wl.worker_grad_bytes_per_step()
     value = worker_bytes / (ms_per_step * 1e-3) / 1e9
-    whole_hbm = sum(job_bytes(j) for j in wl.jobs) / (ms_per_step * 1e-3) / 1e9
+    step_bytes = sum(job_bytes(j) for j in wl.jobs)
+    whole_hbm = step_bytes / (ms_per_step * 1e-3) / 1e9
 
-    # dominant kernel: the job with the most bytes per launch
-    dom = max(range(len(jobs)), key=lambda j: job_bytes(wl.jobs[j]))
-    durs = sorted(ev[dom][s][0].elapsed_time(ev[dom][s][1]) for s in range(K))
-    per_launch_avg_ms = sum(durs) / len(durs)
-    med_ms = durs[len(durs) // 2]
-    # Its average launch duration.  Where the dominant job's kernels run one
-    # after another with nothing else on its stream (one job, or jobs taking
-    # turns on a shared stream): K launches of that job back to back between
-    # one pair of HIP events (an event pair around every launch adds 2-5 us
-    # to each; the spread above comes from those).  With a stream per job the
-    # jobs' launches run concurrently and their streams share the process's
-    # hardware queues, so the stream's time is not the kernel's: the mean of
-    # the per-launch events is taken.
-    if len(jobs) == 1 or shared_stream:
-        djob = jobs[dom]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(djob.stream)
-        for _ in range(K):
-            push(djob)
-            djob.step()
-        e1.record(djob.stream)
-        torch.cuda.synchronize()
-        avg_ms = e0.elapsed_time(e1) / K
-        avg_kind = "K launches back to back on the job's stream between one pair of HIP events"
-    else:
-        avg_ms = per_launch_avg_ms
-        avg_kind = ("mean of HIP event pairs around each launch, the jobs' launches "
-                    "concurrent on their own streams")
-    dom_bytes = job_bytes(wl.jobs[dom])
-    # every job's kernel (mean of its per-launch events)
+    # The kernel: the step's launches of the fused kernel (one per job),
+    # K steps back to back between one pair of HIP events; with several
+    # jobs on their own streams the launches overlap, and the span covers
+    # all of them (span_of_steps).  An event pair around every launch adds
+    # 2-5 us to each, so the per-launch events above serve only for the
+    # spread and for each job's share.
+    # at least 50 ms of launches, so that tiny's microsecond launches are not
+    # dominated by the two events' own cost
+    span_steps = max(K, int(50.0 / max(ms_per_step, 1e-3)))
+    avg_ms = sum(span_of_steps(torch, dev, jobs, push, span_steps, helper))
     per_job = []
     for j, spec in enumerate(wl.jobs):
-        jm = sum(ev[j][s][0].elapsed_time(ev[j][s][1]) for s in range(K)) / K
+        d = sorted(ev[j][s][0].elapsed_time(ev[j][s][1]) for s in range(K))
+        jm = sum(d) / K
         per_job.append({"job": spec.name, "avg_launch_us": round(jm * 1e3, 2),
+                        "median_launch_us": round(d[K // 2] * 1e3, 2),
+                        "min_launch_us": round(d[0] * 1e3, 2),
                         "frac": round(job_bytes(spec) / (jm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
-    achieved = dom_bytes / (avg_ms * 1e-3) / 1e9
-    traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum")
-               else measured_traffic(args.workload))
+    achieved = step_bytes / (avg_ms * 1e-3) / 1e9
+    dom = max(range(len(jobs)), key=lambda j: job_bytes(wl.jobs[j]))
+    traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum" or
+                        args.resident_bytes is not None or args.shared_stream or args.cu_masks)
+               else measured_traffic(wl.name))
     groups, threads, segs, _, _ = jobs[dom].info()
     cached = [job.cached_fraction() for job in jobs]
+    n_any = any(not (s.num_workers <= 16 or s.num_workers in (20, 24, 32)) for s in wl.jobs)
+    kernel = ("aggregate_only + optimize_only" if args.unfused else
+              "fused_step_any" if n_any else "fused_step_fixed")
+    if len(jobs) > 1:
+        kernel += (f" x{len(jobs)} (one launch per job, " +
+                   ("taking turns on one stream)" if shared_stream else "concurrent on their own streams)"))
 
-    ceiling = read_ceiling(torch, dev, grads[dom])
-    cold = cold_launches(torch, dev, jobs, dom, push, args.cold_steps, dom_bytes)
+    ceil = ceilings(torch, dev, grads[dom], states, helper)
+    cold = cold_steps(torch, dev, jobs, push, args.cold_steps, step_bytes, helper)
 
     baseline = None
-    if args.cpu_seconds > 0:
-        baseline = cpu_baseline(wl, grads[0], w0s[0], args.cpu_seconds)
+    if cpu_seconds > 0:
+        baseline = cpu_baseline(wl, grads[0], w0s[0], cpu_seconds)
 
-    out = {
+    frac = achieved / HBM_PEAK_GBS
+    line = {
         "metric": "worker-gradient GB/s aggregated+optimized per step; % of HBM peak",
         "value": round(value, 2),
         "unit": "GB/s",
@@ -698,7 +874,7 @@ def main(argv=None) -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": args.workload,
+            "workload": wl.name,
             "jobs": [{"name": j.name, "workers": j.num_workers, "keys": j.num_keys,
                       "params": j.num_params, "state_cached_fraction": round(r, 4)}
                      for j, r in zip(wl.jobs, cached)],
@@ -711,7 +887,7 @@ def main(argv=None) -> int:
                           {"kind": args.optimizer, "lr": wl.jobs[0].lr,
                            "weight_decay": wl.jobs[0].weight_decay,
                            **({"betas": [0.9, 0.999], "eps": 1e-8} if args.optimizer == "adam" else {})}),
-            "hbm_bytes_per_step": sum(job_bytes(j) for j in wl.jobs),
+            "hbm_bytes_per_step": step_bytes,
             "pushpull": args.pushpull,
             "optimizer_kind": args.optimizer,
             "unfused": args.unfused,
@@ -722,35 +898,37 @@ def main(argv=None) -> int:
             "hbm_pct_of_peak_whole_step": round(100 * whole_hbm / HBM_PEAK_GBS, 2),
             "launch": {"workgroups": groups, "threads": threads, "segments": segs},
             "host_us_per_step": round(host_s * 1e6 / K, 2),
-            "note": NOTES.get(args.workload, ""),
+            "note": NOTES.get(wl.name, ""),
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": ("aggregate_only + optimize_only" if args.unfused else
-                       "fused_step_fixed" if wl.jobs[dom].num_workers <= 16 else "fused_step_any"),
+            "kernel": kernel,
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "frac": round(frac, 4),
             "traffic": traffic,
             "avg_launch_us": round(avg_ms * 1e3, 2),
-            "avg_launch_us_kind": avg_kind,
-            "per_launch_events_us": {"avg": round(per_launch_avg_ms * 1e3, 2),
-                                     "median": round(med_ms * 1e3, 2),
-                                     "min": round(durs[0] * 1e3, 2)},
-            **({"per_job_events": per_job} if len(jobs) > 1 else {}),
-            "measured_read_ceiling": ceiling,
-            "frac_of_read_ceiling": round(achieved / ceiling["GBps"], 4),
+            "avg_launch_us_kind": (f"{span_steps} launches back to back on the job's stream "
+                                   "between one pair of HIP events" if len(jobs) == 1 else
+                                   f"{span_steps} steps of every job back to back between one "
+                                   "pair of HIP events that the job streams wait on and for; "
+                                   "per step"),
+            "per_job_events": per_job,
+            "ceilings": ceil,
+            "frac_of_read_ceiling": round(achieved / ceil["read"]["GBps"], 4),
+            "frac_of_mixed_ceiling": round(achieved / ceil["mixed"]["GBps"], 4),
+            "frac_of_phase_separated": round(achieved / ceil["phase_separated"]["GBps"], 4),
             "cold": cold,
-            "algorithmic_bytes_per_launch": dom_bytes,
+            "algorithmic_bytes_per_launch": step_bytes,
             "kernel_source_hash": kernel_source_hash(),
         },
         "cpu_baseline": baseline,
     }
-    print(json.dumps(out), flush=True)
     for job in jobs:
         job.destroy()
-    return 0
+    del grads, w0s
+    return line
 
 
 if __name__ == "__main__":

@@ -373,6 +373,51 @@ def test_bandwidth_probe_reads_and_leaves_sink(torch_dev):
     assert torch.count_nonzero(sink[64:]).item() == 0
 
 
+def test_write_and_mixed_probes(torch_dev):
+    """The write probe fills its buffers with the value; the mixed probe
+    reads its read buffers and writes its read-write buffers back unchanged,
+    leaving the sink alone unless a sum hits the sentinel; both reject bad
+    arguments."""
+    import ctypes
+    torch, dev = torch_dev
+    from paper_1805_07891_amd import build
+    probe = ctypes.CDLL(build.PROBE_LIB)
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    probe.phub_probe_write.argtypes = [pp, ctypes.c_int, ctypes.c_int64, ctypes.c_int,
+                                       ctypes.c_float, ctypes.c_void_p]
+    probe.phub_probe_mixed.argtypes = [pp, ctypes.c_int, pp, ctypes.c_int, ctypes.c_int64,
+                                       ctypes.c_int, ctypes.c_float, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    tile = probe.phub_probe_tile_elems()
+    n = tile * 5
+    out = [torch.zeros(n + 16, device=dev) for _ in range(2)]
+    optr = (ctypes.c_void_p * 2)(*[b.data_ptr() for b in out])
+    _say("write probe: 2 buffers of", n, "floats, grid 3")
+    assert probe.phub_probe_write(optr, 2, n, 3, 2.5, None) == 0
+    torch.cuda.synchronize()
+    for b in out:
+        assert torch.all(b[:n] == 2.5).item() and not b[n:].any().item()
+    assert probe.phub_probe_write(optr, 2, n + 1, 3, 2.5, None) == -1
+    assert probe.phub_probe_write(optr, 0, n, 3, 2.5, None) == -1
+    reads = [torch.randn(n, device=dev) for _ in range(3)]
+    rw = [torch.randn(n, device=dev) for _ in range(2)]
+    before = [b.clone() for b in rw]
+    rptr = (ctypes.c_void_p * 3)(*[b.data_ptr() for b in reads])
+    wptr = (ctypes.c_void_p * 2)(*[b.data_ptr() for b in rw])
+    sink = torch.zeros(4 * 256, device=dev)
+    _say("mixed probe: 3 read and 2 read-write buffers of", n, "floats, grid 4")
+    assert probe.phub_probe_mixed(rptr, 3, wptr, 2, n, 4, -1.0e30,
+                                  ctypes.c_void_p(sink.data_ptr()), None) == 0
+    torch.cuda.synchronize()
+    for a, b in zip(rw, before):
+        assert torch.equal(a, b)
+    assert torch.count_nonzero(sink).item() == 0
+    assert probe.phub_probe_mixed(rptr, 3, wptr, 2, n + 4, 4, -1.0e30,
+                                  ctypes.c_void_p(sink.data_ptr()), None) == -1
+    assert probe.phub_probe_mixed(rptr, 0, wptr, 0, n, 4, -1.0e30,
+                                  ctypes.c_void_p(sink.data_ptr()), None) == -1
+
+
 @pytest.mark.parametrize("n", [1, 4, 8, 16, 17])
 @pytest.mark.parametrize("nesterov", [True, False])
 def test_unfused_variant_gives_the_same_bits(lib, torch_dev, n, nesterov):

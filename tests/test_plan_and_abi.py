@@ -51,7 +51,8 @@ def test_probe_header_symbols_are_exported():
     with open(os.path.join(ROOT, "include", "phub_probe.h")) as f:
         text = f.read()
     declared = set(re.findall(r"^\s*int\s*(phub_\w+)\s*\(", text, re.M))
-    assert declared == {"phub_probe_read", "phub_probe_tile_elems"}
+    assert declared == {"phub_probe_read", "phub_probe_write", "phub_probe_mixed",
+                        "phub_probe_tile_elems"}
     probe = ctypes.CDLL(build.PROBE_LIB)
     for name in declared:
         assert hasattr(probe, name), name
