@@ -551,9 +551,10 @@ def main(argv=None) -> int:
                     help="budget of the CPU oracle baseline of each other workload (0 skips it)")
     ap.add_argument("--chunk-bytes", type=int, default=None,
                     help="chunk size of the schedule (default: the workload's, 32 KB)")
-    ap.add_argument("--schedule", choices=("lpt", "split"), default="lpt",
-                    help="chunk-to-wave schedule: the paper's balanced partition (lpt) or "
-                         "contiguous, exactly balanced runs (split)")
+    ap.add_argument("--schedule", choices=("lpt", "split", "dynamic"), default="lpt",
+                    help="chunk-to-wave schedule: the paper's balanced partition (lpt), "
+                         "contiguous, exactly balanced runs (split), or lpt with the streamed "
+                         "tiles taken by the waves from a shared counter (dynamic)")
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
@@ -733,7 +734,7 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
     line."""
     from paper_1805_07891_amd import workloads
     from paper_1805_07891_amd.job import TorchJob
-    from paper_1805_07891_amd.phub import PHUB_SCHEDULE_SPLIT
+    from paper_1805_07891_amd.phub import PHUB_SCHEDULE_DYNAMIC, PHUB_SCHEDULE_SPLIT
 
     # Co-running jobs each have their own stream (their launches run
     # concurrently); with --shared-stream they take turns on one stream,
@@ -748,7 +749,8 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
         job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
                        chunk_bytes=args.chunk_bytes, unfused=args.unfused,
                        optimizer=None if args.optimizer == "momentum" else args.optimizer,
-                       schedule=None if args.schedule == "lpt" else PHUB_SCHEDULE_SPLIT,
+                       schedule={"lpt": None, "split": PHUB_SCHEDULE_SPLIT,
+                                 "dynamic": PHUB_SCHEDULE_DYNAMIC}[args.schedule],
                        workgroups=masked[ji][1] if masked is not None else args.workgroups)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)

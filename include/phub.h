@@ -85,8 +85,15 @@ int phub_init(phub_job **out, int num_workers, int num_keys, const int64_t *key_
 
 /* Chunk-to-wave schedules (section 3.2.4; see the schedule section below). */
 enum phub_schedule {
-    PHUB_SCHEDULE_SPLIT = 0, /* contiguous, exactly balanced runs of chunks */
-    PHUB_SCHEDULE_LPT = 1    /* the paper's balanced partition of chunks (default) */
+    PHUB_SCHEDULE_SPLIT = 0,  /* contiguous, exactly balanced runs of chunks */
+    PHUB_SCHEDULE_LPT = 1,    /* the paper's balanced partition of chunks (default) */
+    PHUB_SCHEDULE_DYNAMIC = 2 /* phub_init_ex only: the LPT schedule, except that the
+                                 streamed state's full 1024-element tiles are not fixed
+                                 per wave: each launch's waves take them one at a time,
+                                 in address order, from a counter they share (work
+                                 stealing), so that waves that start late take fewer.
+                                 Kept for jobs with a fixed-N kernel (1-16, 20, 24 or
+                                 32 workers, fused); others run as LPT. */
 };
 
 /* Optimizers (section 3.2.2: aggregators and optimizers are pluggable).

@@ -205,7 +205,9 @@ __device__ __forceinline__ uint32_t wave_index() {
         const DevRem* __restrict__ rems, const int32_t* __restrict__ rem_begin,           \
         const float* const* __restrict__ grads, float* const* __restrict__ outs,          \
         float* __restrict__ weights, float* __restrict__ moments,                         \
-        float* __restrict__ second, OptArgs o, int num_workers
+        float* __restrict__ second, OptArgs o, int num_workers,                           \
+        const DevTile* __restrict__ pool, int32_t pool_count,                             \
+        unsigned long long* __restrict__ pool_counters, PoolBases pool_bases
 
 // Splits a tile's float4 index into a part folded into the base pointers
 // (a multiple of 2^20 float4, 16 MB) and a low part that keeps the per-lane
@@ -513,6 +515,61 @@ __device__ __forceinline__ void tile_prologue(std::integer_sequence<int, I...>,
     ((p.ring[I % kRing<NW, S, RES>] = tile_load<NW, S, RES, I>(a)), ...);
 }
 
+// ------------------------------------------------------ the tile pool
+
+// Dynamic schedule (work stealing): the streamed bin's full tiles of a
+// launch form one pool, in address order, and every wave takes its next
+// tile of the pool from a counter shared with the other waves of its XCD
+// (PoolCounters), each counter serving every C-th tile, so that all waves
+// still work on neighbouring tiles.  A wave that starts late (its compute
+// unit was still held by another tenant's launch) simply takes fewer
+// tiles.  A counter is never reset: the host passes each launch the
+// counter's value at its start (the base), and every wave stops after
+// exactly one take past its tiles.
+//
+// A take is a vector atomic from lane 0 whose value is read one tile later
+// (issue_take, then resolve_take), so that the wait for it falls behind
+// loads the wave has issued meanwhile, not in front of them.
+__device__ __forceinline__ uint64_t issue_take(unsigned long long* counter) {
+    uint64_t v = 0;
+    if ((threadIdx.x & 63u) == 0) v = atomicAdd(counter, 1ull);
+    return v;
+}
+
+// Pool index of a take, or -1 past the pool (or before it: never, unless
+// the base is wrong, in which case nothing is read).
+__device__ __forceinline__ int32_t resolve_take(uint64_t v, uint64_t base, int32_t count) {
+    const uint32_t lo = uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(v))));
+    const uint32_t hi = uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(v >> 32))));
+    const int64_t i = int64_t(((uint64_t(hi) << 32) | lo) - base);
+    return i >= 0 && i < int64_t(count) ? int32_t(i) : -1;
+}
+
+// Writes back the stashed state of the first `used` stash slots, slot i
+// holding pool tile pool[idx[i] * stride] (burst write-back of the pool
+// walk).
+template <int NW, int S, int SLOTS>
+__device__ __forceinline__ void write_stash_slots(const DevTile* __restrict__ pool, int stride,
+                                                  const int32_t (&idx)[SLOTS], int used,
+                                                  const PHUB_LDS f4* stash, float* const* state) {
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k) {
+        if (k < used) {
+            TileStreams<NW, S> s;
+            tile_bases<NW, S>(s, pool[int64_t(idx[k]) * stride], state);
+            const PHUB_LDS f4* ts = stash + k * kStashTileVecs<S>;
+#pragma unroll
+            for (int i = 0; i < S; ++i) {
+#pragma unroll
+                for (int u = 0; u < kVecPerLane; ++u) {
+                    const f4 v = ts[(i * kVecPerLane + u) * 64];
+                    store_wm<false>(s.st[i], s.off + u * 1024u, v);
+                }
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------ remainders
 
 // The rest of a segment: nvec < 256 float4 then a ragged end of rem < 4
@@ -623,6 +680,85 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
     }
 }
 
+// The streamed full tiles of a launch taken from its pool (dynamic
+// schedule), NW workers: walk_tiles' pipeline, with the next tiles known
+// from takes instead of a fixed list.  The wave's counter serves the pool
+// tiles pool[i * stride], i < count.  At the start of tile t the wave
+// resolves the take of tile t + 2 (issued at the start of tile t - 1),
+// fetches that tile's descriptor and issues the take of tile t + 3 (only
+// while takes still land in the pool).
+template <int NW, int OPT, bool PULL>
+__device__ __forceinline__ void walk_pool(const DevTile* __restrict__ pool, int32_t count,
+                                          int stride, unsigned long long* counter, uint64_t base,
+                                          const float* const* __restrict__ grads,
+                                          float* const* __restrict__ outs, float* const* state,
+                                          OptArgs o, PHUB_LDS f4* stash) {
+    constexpr bool RES = false;
+    constexpr int S = kStates<OPT>;
+    constexpr int NPH = kPhases<NW, S, RES>;
+    static_assert(NPH >= 1 && NPH <= 3, "the tile loop below unrolls at most three phases");
+    constexpr bool STASH = kStash<NW, S, RES, PULL>;
+    constexpr int SLOTS = STASH ? kStashTiles<S> : 1;
+    int32_t cur = resolve_take(issue_take(counter), base, count);
+    if (cur < 0) return;
+    int32_t n1 = resolve_take(issue_take(counter), base, count);
+    bool take2 = n1 >= 0;  // a take of the tile after next is in flight
+    uint64_t v2 = take2 ? issue_take(counter) : 0;
+    TilePipe<NW, S, RES> p;
+    TileStreams<NW, S> a, b;
+    uint64_t prow = 0;
+    {
+        const DevTile first = pool[int64_t(cur) * stride];
+        tile_streams<NW, S>(a, first, grads + int64_t(first.key) * NW, state);
+        if constexpr (PULL) prow = load_row<NW>(outs + int64_t(first.key) * NW);
+    }
+    DevTile nd = pool[int64_t(n1 >= 0 ? n1 : cur) * stride];
+    tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
+    int32_t slot[SLOTS];  // burst write-back: pool tiles whose state waits in the stash
+    int used = 0;
+    auto one_tile = [&](auto phase) -> bool {
+        constexpr int PH = decltype(phase)::value;
+        const bool has_next = n1 >= 0;
+        const uint64_t nrow = load_row<NW>(grads + int64_t(nd.key) * NW);
+        uint64_t nprow = 0;
+        if constexpr (PULL) nprow = load_row<NW>(outs + int64_t(nd.key) * NW);
+        const int32_t n2 = take2 ? resolve_take(v2, base, count) : -1;
+        const bool take3 = n2 >= 0;
+        const uint64_t v3 = take3 ? issue_take(counter) : 0;
+        const DevTile nd2 = pool[int64_t(n2 >= 0 ? n2 : cur) * stride];
+        PHUB_LDS f4* tile_stash = nullptr;  // this tile's slot of the stash
+        if constexpr (STASH) tile_stash = stash + used * kStashTileVecs<S>;
+        tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
+                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash);
+        if constexpr (STASH) {
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k)
+                if (k == used) slot[k] = cur;
+            ++used;
+            if (used == SLOTS || !has_next || in_write_window(o.wb_period, o.wb_window)) {
+                write_stash_slots<NW, S, SLOTS>(pool, stride, slot, used, stash, state);
+                used = 0;
+            }
+        }
+        if (!has_next) return false;
+        a = b;
+        nd = nd2;
+        prow = nprow;
+        cur = n1;
+        n1 = n2;
+        take2 = take3;
+        v2 = v3;
+        return true;
+    };
+    for (;;) {
+        if (!one_tile(std::integral_constant<int, 0>{})) break;
+        if constexpr (NPH >= 2)
+            if (!one_tile(std::integral_constant<int, 1 % NPH>{})) break;
+        if constexpr (NPH >= 3)
+            if (!one_tile(std::integral_constant<int, 2 % NPH>{})) break;
+    }
+}
+
 // The remainders [rb, re) of one bin.
 template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void walk_rems(const DevRem* __restrict__ rems, int32_t rb, int32_t re,
@@ -668,8 +804,17 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
         stash = (PHUB_LDS f4*)stash_lds +
                 (threadIdx.x >> 6) * (kStashTiles<S> * kStashTileVecs<S>) + (threadIdx.x & 63u);
     }
-    walk_tiles<NW, OPT, false, PULL>(tiles, tile_begin[bins + wave], tile_begin[bins + wave + 1],
-                                     grads, outs, state, o, stash);
+    if (pool_count > 0) {
+        // this workgroup's counter and the pool tiles it serves
+        const int nc = pool_bases.counters;
+        const int c = int(blockIdx.x % uint32_t(nc));
+        walk_pool<NW, OPT, PULL>(pool + c, int32_t(pool_counter_tiles(pool_count, c, nc)), nc,
+                                 pool_counters + c * kPoolCounterStride, pool_bases.base[c], grads,
+                                 outs, state, o, stash);
+    } else {
+        walk_tiles<NW, OPT, false, PULL>(tiles, tile_begin[bins + wave],
+                                         tile_begin[bins + wave + 1], grads, outs, state, o, stash);
+    }
     walk_tiles<NW, OPT, true, PULL>(tiles, tile_begin[wave], tile_begin[wave + 1], grads, outs,
                                     state, o, stash);
     walk_rems<NW, OPT, true, PULL>(rems, rem_begin[wave], rem_begin[wave + 1], grads, outs, state,
@@ -915,7 +1060,7 @@ __global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS,
 
 #define PHUB_LAUNCH_ARGS                                                                     \
     p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.outs, p.weights, p.moments,        \
-        p.second, p.opt, p.num_workers
+        p.second, p.opt, p.num_workers, p.pool, p.pool_count, p.pool_counters, p.pool_bases
 
 template <int OPT, bool PULL>
 hipError_t launch_any(const StepParams& p, int grid, hipStream_t stream) {
@@ -984,7 +1129,54 @@ hipError_t launch_opt(const StepParams& p, int grid, hipStream_t stream) {
 
 }  // namespace
 
+namespace {
+
+template <int NW, int S>
+constexpr bool fixed_launchable() {
+    return kPhases<NW, S, true> <= 3 && kPhases<NW, S, false> <= 3;
+}
+
+template <int S>
+bool fixed_launchable_n(int n) {
+    switch (n) {
+        case 1: return fixed_launchable<1, S>();
+        case 2: return fixed_launchable<2, S>();
+        case 3: return fixed_launchable<3, S>();
+        case 4: return fixed_launchable<4, S>();
+        case 5: return fixed_launchable<5, S>();
+        case 6: return fixed_launchable<6, S>();
+        case 7: return fixed_launchable<7, S>();
+        case 8: return fixed_launchable<8, S>();
+        case 9: return fixed_launchable<9, S>();
+        case 10: return fixed_launchable<10, S>();
+        case 11: return fixed_launchable<11, S>();
+        case 12: return fixed_launchable<12, S>();
+        case 13: return fixed_launchable<13, S>();
+        case 14: return fixed_launchable<14, S>();
+        case 15: return fixed_launchable<15, S>();
+        case 16: return fixed_launchable<16, S>();
+        case 20: return fixed_launchable<20, S>();
+        case 24: return fixed_launchable<24, S>();
+        case 32: return fixed_launchable<32, S>();
+        default: return false;
+    }
+}
+
+}  // namespace
+
+bool takes_tile_pool(int num_workers, int optimizer) {
+    switch (optimizer) {
+        case kOptMomentum:
+        case kOptNesterov: return fixed_launchable_n<2>(num_workers);
+        case kOptSgd: return fixed_launchable_n<1>(num_workers);
+        case kOptAdam: return fixed_launchable_n<3>(num_workers);
+        default: return false;
+    }
+}
+
 hipError_t launch_fused_step(const StepParams& p, int optimizer, int grid, hipStream_t stream) {
+    if (p.pool_count > 0 && (p.merge || !takes_tile_pool(p.num_workers, optimizer)))
+        return hipErrorInvalidValue;  // only the fixed-N fused kernels walk a pool
     switch (optimizer) {
         case kOptMomentum: return launch_opt<kOptMomentum>(p, grid, stream);
         case kOptNesterov: return launch_opt<kOptNesterov>(p, grid, stream);

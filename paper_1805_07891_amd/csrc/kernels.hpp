@@ -104,6 +104,31 @@ inline void write_phase_ticks(int num_workers, int num_states, int64_t clock_khz
     *window = uint32_t(std::min<int64_t>(std::max<int64_t>(w, 1), *period - 1));
 }
 
+// Counters of the dynamic schedule.  The waves of workgroup g take from
+// counter g mod C (C = the launch's counters, at most kMaxPoolCounters and
+// at most its workgroups: one per XCD of MI355X, whose workgroups go to the
+// XCDs in turn), counter c serving pool tiles c, c + C, c + 2 C, ...  Each
+// counter sits on its own 256-byte line.  A counter is never reset: a launch
+// passes each counter's value at its start (base) and adds to it the tiles
+// it serves plus its waves (each wave takes once past its tiles).
+constexpr int kMaxPoolCounters = 8;
+constexpr int kPoolCounterStride = 32;  // unsigned long long: 256 bytes
+
+struct PoolBases {
+    uint64_t base[kMaxPoolCounters];
+    int32_t counters;  // C
+};
+
+// Tiles of a pool of `count` tiles that counter c of C serves.
+constexpr int64_t pool_counter_tiles(int64_t count, int c, int counters) {
+    return count > c ? (count - c + counters - 1) / counters : 0;
+}
+
+// Workgroups of a grid of `grid` that take from counter c of C.
+constexpr int64_t pool_counter_groups(int64_t grid, int c, int counters) {
+    return grid > c ? (grid - c + counters - 1) / counters : 0;
+}
+
 // Scalars of one launch.  For Adam, c1 = 1 - b1, c2 = 1 - b2 and the
 // step's bias corrections k1 = lr / (1 - b1^t), k2 = 1 / (1 - b2^t) are
 // computed on the host in double and rounded to fp32 once.
@@ -138,7 +163,18 @@ struct StepParams {
     float* second;                // V arena (Adam's second moment), or null
     OptArgs opt;
     int num_workers;
+    // dynamic schedule: the launch's streamed full tiles as one pool (the
+    // streamed bins then hold only remainders), taken by the waves through
+    // pool counters (see PoolCounters).  pool_count 0: none.
+    const DevTile* pool;
+    int32_t pool_count;
+    unsigned long long* pool_counters;  // kMaxPoolCounters counters, kPoolCounterStride apart
+    PoolBases pool_bases;
 };
+
+// Whether the fused kernel for num_workers and optimizer (an OptKind) can
+// walk a tile pool (the fixed-N kernels; not the any-N kernel).
+bool takes_tile_pool(int num_workers, int optimizer);
 
 // A part of a key scheduled on its own (a job's cache-resident or
 // streamed part of the key): the key's row in the gradient pointer table,

@@ -65,6 +65,8 @@ namespace {
 constexpr int kStageSlots = 4;       // pinned staging buffers for pointer-table uploads
 constexpr int kMaxWorkgroups = 1 << 16;  // largest persistent grid a job may ask for
 constexpr int64_t kArenaAlign = 64;  // elements: 256-byte aligned key slices
+constexpr size_t kCounterBytes =
+    size_t(phub::kMaxPoolCounters) * phub::kPoolCounterStride * sizeof(unsigned long long);
 
 thread_local std::string g_error;
 
@@ -108,6 +110,7 @@ struct phub_job {
     bool own_stream = false;
 
     int schedule = phub::kScheduleLpt;
+    bool dynamic = false;  // the streamed full tiles are taken from a pool (PHUB_SCHEDULE_DYNAMIC)
     int groups = 0;  // workgroups of one launch (0: no key has elements)
     int bins = 0;    // waves with a segment list (groups * waves per workgroup)
     int64_t num_segments = 0;
@@ -142,6 +145,10 @@ struct phub_job {
     int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of 2 * bins + 1 entries
     phub::DevRem* d_rems = nullptr;
     int32_t* d_rem_begin = nullptr;   // same layout
+    std::vector<int32_t> pool_begin;  // per readiness group: its tile pool in d_tiles
+    std::vector<int32_t> pool_count;  // (0: the group's schedule is static)
+    unsigned long long* d_counters = nullptr;  // takes from the pools (never reset)
+    uint64_t counter_next[phub::kMaxPoolCounters] = {};  // their values when the next launch starts
     const float** d_grads = nullptr;  // [row * N + worker]
     float** d_outs = nullptr;         // same layout: pushpull model buffers
 
@@ -196,6 +203,7 @@ void release(phub_job* j) {
     if (j->d_tiles) (void)hipFree(j->d_tiles);
     if (j->d_rem_begin) (void)hipFree(j->d_rem_begin);
     if (j->d_rems) (void)hipFree(j->d_rems);
+    if (j->d_counters) (void)hipFree(j->d_counters);
     if (j->moments) (void)hipFree(j->moments);
     if (j->second) (void)hipFree(j->second);
     if (j->merge) (void)hipFree(j->merge);
@@ -366,8 +374,23 @@ int launch_group(phub_job* j, int g) {
         p.second = j->second;
         p.opt = optimizer_args(j);
         p.num_workers = j->num_workers;
+        const int32_t pool = j->pool_count.empty() ? 0 : j->pool_count[g];
+        const int counters = std::min(phub::kMaxPoolCounters, j->groups);
+        if (pool > 0) {
+            p.pool = j->d_tiles + j->pool_begin[g];
+            p.pool_count = pool;
+            p.pool_counters = j->d_counters;
+            p.pool_bases.counters = counters;
+            for (int c = 0; c < counters; ++c) p.pool_bases.base[c] = j->counter_next[c];
+        }
         hipError_t e = phub::launch_fused_step(p, j->opt, j->groups, j->stream);
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
+        // each counter serves its tiles, and each of its waves takes once past them
+        if (pool > 0)
+            for (int c = 0; c < counters; ++c)
+                j->counter_next[c] += uint64_t(phub::pool_counter_tiles(pool, c, counters)) +
+                                      uint64_t(phub::kBlockThreads / 64) *
+                                          uint64_t(phub::pool_counter_groups(j->groups, c, counters));
     }
     j->rgroup_launched[g] = 1;
     return PHUB_OK;
@@ -536,7 +559,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             return fail(PHUB_EINVAL, "workgroups must be in [0, %d], got %d", kMaxWorkgroups,
                         options->workgroups);
         workgroups = options->workgroups;
-        if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT)
+        if (options->schedule != PHUB_SCHEDULE_SPLIT && options->schedule != PHUB_SCHEDULE_LPT &&
+            options->schedule != PHUB_SCHEDULE_DYNAMIC)
             return fail(PHUB_EINVAL, "unknown schedule %d", options->schedule);
         if (options->resident_bytes < -1)
             return fail(PHUB_EINVAL, "resident_bytes must be >= -1, got %lld",
@@ -719,8 +743,10 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                         std::vector<int64_t> elems(vk.size());
                         for (size_t i = 0; i < vk.size(); ++i) elems[i] = vk[i].elems;
                         err = phub::build_plan(num_workers, int(vk.size()), elems.data(),
-                                               chunk_bytes, schedule, bins,
-                                               kLptItemsPerBin * bins, &plan);
+                                               chunk_bytes,
+                                               schedule == PHUB_SCHEDULE_DYNAMIC ? phub::kScheduleLpt
+                                                                                : schedule,
+                                               bins, kLptItemsPerBin * bins, &plan);
                     } else {
                         plan.bin_begin.assign(1, 0);
                     }
@@ -746,6 +772,9 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         j->bins = bins;
     }
     j->schedule = schedule;
+    // the pool walk exists in the fixed-N fused kernels only
+    j->dynamic = schedule == PHUB_SCHEDULE_DYNAMIC && !unfused && j->groups > 0 &&
+                 phub::takes_tile_pool(num_workers, j->opt);
     const int num_states = j->num_states;
 
 #define PHUB_TRY(call, what)                 \
@@ -799,6 +828,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                 dt.tile_begin.push_back(int32_t(dt.tiles.size()));
                 dt.rem_begin.push_back(int32_t(dt.rems.size()));
                 for (int ph = 0; ph < 2; ++ph) {
+                    const size_t t0 = dt.tiles.size();
                     const int64_t elems = phub::append_device_tables(
                         plans[g * 2 + ph], vkeys[g * 2 + ph], row_arena_offset, j->bins, &dt);
                     if (elems < 0) {
@@ -806,6 +836,17 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                         goto fail_cleanup;
                     }
                     if (ph == 0) j->resident_bytes += elems * elem_state_bytes;
+                    if (ph == 1 && j->dynamic) {
+                        // the streamed full tiles become the group's pool, in
+                        // address order; its bins keep their remainders only
+                        std::sort(dt.tiles.begin() + t0, dt.tiles.end(),
+                                  [](const phub::DevTile& x, const phub::DevTile& y) {
+                                      return x.arena_offset < y.arena_offset;
+                                  });
+                        j->pool_begin.push_back(int32_t(t0));
+                        j->pool_count.push_back(int32_t(dt.tiles.size() - t0));
+                        std::fill(dt.tile_begin.end() - j->bins, dt.tile_begin.end(), int32_t(t0));
+                    }
                 }
             }
         }
@@ -825,7 +866,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             hipMalloc(&j->d_rems, rem_bytes) != hipSuccess ||
             hipMalloc(&j->d_rem_begin, rb_bytes) != hipSuccess ||
             hipMalloc(&j->d_grads, tab_bytes) != hipSuccess ||
-            hipMalloc(&j->d_outs, tab_bytes) != hipSuccess) {
+            hipMalloc(&j->d_outs, tab_bytes) != hipSuccess ||
+            (j->dynamic && hipMalloc(&j->d_counters, kCounterBytes) != hipSuccess)) {
             (void)hipGetLastError();
             rc = fail(PHUB_ENOMEM, "device allocation of the schedule failed");
             goto fail_cleanup;
@@ -840,6 +882,9 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                      "hipMemcpy(remainders)");
         PHUB_TRY(hipMemcpy(j->d_tile_begin, tile_begin.data(), tb_bytes, hipMemcpyHostToDevice),
                  "hipMemcpy(tile bins)");
+        if (j->d_counters)
+            PHUB_TRY(hipMemsetAsync(j->d_counters, 0, kCounterBytes, j->stream),
+                     "hipMemsetAsync(pool counters)");
         PHUB_TRY(hipMemcpy(j->d_rem_begin, rem_begin.data(), rb_bytes, hipMemcpyHostToDevice),
                  "hipMemcpy(remainder bins)");
         for (int i = 0; i < kStageSlots; ++i) {

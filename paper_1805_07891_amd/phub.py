@@ -29,6 +29,7 @@ STATUS_NAMES = {0: "PHUB_OK", -1: "PHUB_EINVAL", -2: "PHUB_ENOTREADY", -3: "PHUB
 
 PHUB_SCHEDULE_SPLIT = 0
 PHUB_SCHEDULE_LPT = 1
+PHUB_SCHEDULE_DYNAMIC = 2
 
 PHUB_OPT_MOMENTUM = 0
 PHUB_OPT_SGD = 1

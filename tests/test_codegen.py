@@ -104,3 +104,16 @@ def test_gradient_loads_are_non_temporal(asm):
         loads = re.findall(r"^\s+global_load_dwordx4\b.*$", _body(asm, name), re.M)
         nt = [line for line in loads if re.search(r"\bnt\b", line)]
         assert loads and nt, name
+
+
+def test_the_only_atomics_are_vector_atomics_of_the_dynamic_schedule(asm):
+    """The dynamic schedule's takes are vector atomics from one lane (the
+    only read-modify-write the kernels do); no other kind appears."""
+    meta = _kernels(asm)
+    for name in meta:
+        ops = {m.split()[0] for m in re.findall(r"^\s+(\S*atomic\S*)", _body(asm, name), re.M)}
+        if "fused_step_fixed" in name:
+            assert ops == {"global_atomic_add_x2"}, (name, ops)
+        else:
+            assert not ops, (name, ops)
+

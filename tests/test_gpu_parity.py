@@ -180,7 +180,8 @@ def test_chunk_size_does_not_change_results(lib, torch_dev):
             assert _bits_equal(wg[k], outs[0][0][k]) and _bits_equal(mg[k], outs[0][1][k])
 
 
-@pytest.mark.parametrize("schedule", [phub.PHUB_SCHEDULE_SPLIT, phub.PHUB_SCHEDULE_LPT])
+@pytest.mark.parametrize("schedule", [phub.PHUB_SCHEDULE_SPLIT, phub.PHUB_SCHEDULE_LPT,
+                                      phub.PHUB_SCHEDULE_DYNAMIC])
 @pytest.mark.parametrize("resident", [0, 4096, 1 << 20, 8 * 150001, 1 << 40])
 def test_schedule_and_cache_residency_do_not_change_results(lib, torch_dev, schedule, resident):
     torch, dev = torch_dev

@@ -40,11 +40,11 @@ def _bits_equal(a, b):
 
 class Case:
     def __init__(self, torch, dev, lib, n_workers, key_elems, seed, key_group=None,
-                 resident_bytes=None, nesterov=True):
+                 resident_bytes=None, nesterov=True, schedule=None):
         self.torch = torch
         self.spec = Job("pushpull", n_workers, tuple(int(n) for n in key_elems), nesterov=nesterov)
         self.job = TorchJob(self.spec, dev, lib=lib, key_group=key_group,
-                            resident_bytes=resident_bytes)
+                            resident_bytes=resident_bytes, schedule=schedule)
         self.offs, self.total = key_offsets(self.spec.key_elems)
         self.rng = np.random.default_rng(seed)
         w0 = np.zeros(self.total, np.float32)
@@ -93,10 +93,13 @@ KEYS = (5, 1024, 8193, 40000, 3, 70001, 2048, 131072, 1)
 
 @pytest.mark.parametrize("n_workers", [1, 4, 8, 16, 17])
 @pytest.mark.parametrize("resident", [0, 8 * 50000, 1 << 40])
-def test_pushpull_writes_the_updated_weights_to_every_worker(lib, torch_dev, n_workers, resident):
+@pytest.mark.parametrize("schedule", [None, phub.PHUB_SCHEDULE_DYNAMIC])
+def test_pushpull_writes_the_updated_weights_to_every_worker(lib, torch_dev, n_workers, resident,
+                                                             schedule):
     torch, dev = torch_dev
-    _say("pushpull N", n_workers, "resident", resident)
-    c = Case(torch, dev, lib, n_workers, KEYS, seed=21 + n_workers, resident_bytes=resident)
+    _say("pushpull N", n_workers, "resident", resident, "schedule", schedule)
+    c = Case(torch, dev, lib, n_workers, KEYS, seed=21 + n_workers, resident_bytes=resident,
+             schedule=schedule)
     for t in range(2):
         host, arenas = c.new_grads()
         c.job.pushpull_all()

@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
+from paper_1805_07891_amd import phub
 from paper_1805_07891_amd.job import TorchJob, load_library
 from paper_1805_07891_amd.workloads import Job, key_offsets
 
@@ -55,16 +56,17 @@ def _bits_equal(a, b):
                           np.asarray(b, np.float32).view(np.uint32))
 
 
-def _run(lib, torch_dev, n, opt, workgroups, resident, key_group=None):
+def _run(lib, torch_dev, n, opt, workgroups, resident, key_group=None, schedule=None):
     torch, dev = torch_dev
     states = {"sgd": 1, "adam": 3}.get(opt, 2)
     if resident == "partial":
         resident = 4 * states * 50000
-    _say("stash", opt, "N", n, "workgroups", workgroups, "resident", resident, "groups", key_group)
+    _say("stash", opt, "N", n, "workgroups", workgroups, "resident", resident, "groups", key_group,
+         "schedule", schedule)
     spec = Job("stash", n, KEYS, lr=LR, momentum=MU, weight_decay=WD, nesterov=opt == "nesterov")
     job = TorchJob(spec, dev, lib=lib, resident_bytes=resident, workgroups=workgroups,
                    optimizer={"momentum": None, "nesterov": None}.get(opt, opt), betas=(B1, B2),
-                   eps=EPS, key_group=key_group)
+                   eps=EPS, key_group=key_group, schedule=schedule)
     offs, total = key_offsets(KEYS)
     rng = np.random.default_rng(1000 + n)
     w0 = np.zeros(total, np.float32)
@@ -137,3 +139,17 @@ def test_larger_fixed_worker_counts(lib, torch_dev, n, opt, workgroups, resident
     burst write-back, resident ring below a whole tile); bit-exact against
     the oracle like the others."""
     _run(lib, torch_dev, n, opt, workgroups, resident)
+
+
+@pytest.mark.parametrize("n,opt", [(8, "nesterov"), (16, "momentum"), (4, "nesterov"), (11, "sgd"),
+                                   (14, "adam"), (3, "adam"), (24, "momentum")])
+@pytest.mark.parametrize("workgroups,resident", [(1, 0), (3, 0), (5, "partial"), (None, 0)])
+@pytest.mark.parametrize("grouped", [False, True])
+def test_dynamic_schedule_matches_the_oracle(lib, torch_dev, n, opt, workgroups, resident, grouped):
+    """The dynamic schedule: the streamed full tiles taken from a pool by the
+    waves (with and without burst write-back), every launch of a step
+    (readiness groups) and of the next step advancing the shared counter;
+    bit-exact against the oracle over two steps."""
+    _run(lib, torch_dev, n, opt, workgroups, resident,
+         key_group=[k % 3 for k in range(len(KEYS))] if grouped else None,
+         schedule=phub.PHUB_SCHEDULE_DYNAMIC)
