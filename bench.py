@@ -549,12 +549,20 @@ def main(argv=None) -> int:
                     help="budget of the CPU oracle baseline of the headline workload (0 skips it)")
     ap.add_argument("--config-cpu-seconds", type=float, default=2.0,
                     help="budget of the CPU oracle baseline of each other workload (0 skips it)")
+    ap.add_argument("--min-timed-ms", type=float, default=0.0,
+                    help="time at least this long: more than --steps steps where a step is "
+                         "short (the five-workload run passes 50 to every workload but the "
+                         "headline, which always times exactly --steps)")
     ap.add_argument("--chunk-bytes", type=int, default=None,
                     help="chunk size of the schedule (default: the workload's, 32 KB)")
     ap.add_argument("--schedule", choices=("lpt", "split", "dynamic"), default="lpt",
                     help="chunk-to-wave schedule: the paper's balanced partition (lpt), "
                          "contiguous, exactly balanced runs (split), or lpt with the streamed "
                          "tiles taken by the waves from a shared counter (dynamic)")
+    ap.add_argument("--whole-chunks", action="store_true",
+                    help="ablation: chunks of --chunk-bytes are indivisible items of the "
+                         "schedule, as in the paper (by default they are split while there are "
+                         "fewer than 128 items per wave)")
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
@@ -657,7 +665,13 @@ def main(argv=None) -> int:
 
 
 # Flags main() handles itself and does not pass on to a workload's process.
-_OWN_FLAGS = {"--workload": 1, "--cpu-seconds": 1, "--config-cpu-seconds": 1}
+_OWN_FLAGS = {"--workload": 1, "--cpu-seconds": 1, "--config-cpu-seconds": 1, "--min-timed-ms": 1}
+
+# Shortest timed region of the workloads other than the headline: with the
+# driver's 20 steps the tiny workload's 5 us steps make 0.1 ms of work, and
+# the two synchronisations around it (about 3 us each, plus the queue's
+# start) would count as a third of it.
+CONFIG_MIN_TIMED_MS = 50.0
 
 
 def run_all(args, argv) -> int:
@@ -688,6 +702,8 @@ def run_all(args, argv) -> int:
         budget = args.cpu_seconds if name == HEADLINE_WORKLOAD else args.config_cpu_seconds
         cmd = [sys.executable, "-u", os.path.abspath(__file__), "--workload", name,
                "--cpu-seconds", str(budget), *passed]
+        if name != HEADLINE_WORKLOAD:
+            cmd += ["--min-timed-ms", str(CONFIG_MIN_TIMED_MS)]
         print(f"bench: {name}", file=sys.stderr, flush=True)
         r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
         if r.returncode != 0:
@@ -751,7 +767,8 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
                        optimizer=None if args.optimizer == "momentum" else args.optimizer,
                        schedule={"lpt": None, "split": PHUB_SCHEDULE_SPLIT,
                                  "dynamic": PHUB_SCHEDULE_DYNAMIC}[args.schedule],
-                       workgroups=masked[ji][1] if masked is not None else args.workgroups)
+                       workgroups=masked[ji][1] if masked is not None else args.workgroups,
+                       whole_chunks=args.whole_chunks)
         w0 = workloads.device_weight_arena(torch, dev, spec, wl.seed_index, ji)
         g = [workloads.device_grad_arena(torch, dev, spec, wl.seed_index, ji, 0, w)
              for w in range(spec.num_workers)]
@@ -780,6 +797,16 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
     torch.cuda.synchronize()
 
     K = args.steps
+    if args.min_timed_ms > 0:
+        # the step's time, from 50 more untimed steps
+        tw = time.perf_counter()
+        for _ in range(50):
+            for job in jobs:
+                push(job)
+                job.step()
+        torch.cuda.synchronize()
+        est_ms = (time.perf_counter() - tw) * 1e3 / 50
+        K = max(K, int(args.min_timed_ms / max(est_ms, 1e-4)) + 1)
     # Timed region: K steps of every job, wall clock between two device
     # synchronizations, with nothing else on the streams.
     torch.cuda.synchronize()
@@ -843,7 +870,8 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
     achieved = step_bytes / (avg_ms * 1e-3) / 1e9
     dom = max(range(len(jobs)), key=lambda j: job_bytes(wl.jobs[j]))
     traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum" or
-                        args.resident_bytes is not None or args.shared_stream or args.cu_masks)
+                        args.resident_bytes is not None or args.shared_stream or args.cu_masks or
+                        args.whole_chunks or args.schedule != "lpt" or args.chunk_bytes)
                else measured_traffic(wl.name))
     groups, threads, segs, _, _ = jobs[dom].info()
     cached = [job.cached_fraction() for job in jobs]
@@ -882,6 +910,7 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
                      for j, r in zip(wl.jobs, cached)],
             "chunk_bytes": args.chunk_bytes or wl.jobs[0].chunk_bytes,
             "schedule": args.schedule,
+            "whole_chunks": args.whole_chunks,
             "workgroups_option": args.workgroups,
             "optimizer": ({"lr": wl.jobs[0].lr, "momentum": wl.jobs[0].momentum,
                            "weight_decay": wl.jobs[0].weight_decay, "nesterov": wl.jobs[0].nesterov}

@@ -178,6 +178,14 @@ typedef struct phub_options {
                                distinct event is waited for.  Either way,
                                events already complete when the launch is
                                enqueued are not waited for. */
+    int whole_chunks;       /* ablation of the chunk size (section 3.2.3):
+                               1 keeps every chunk of chunk_bytes an
+                               indivisible item of the LPT schedule, as in
+                               the paper (no splitting of chunks however few
+                               they are).  0 (default): while there are fewer
+                               than 128 items per wave, chunks are halved, not
+                               below 1024 elements, so that every wave has
+                               work.  Results do not depend on it. */
 } phub_options;
 
 /*

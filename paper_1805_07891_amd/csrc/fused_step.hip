@@ -207,7 +207,7 @@ __device__ __forceinline__ uint32_t wave_index() {
         float* __restrict__ weights, float* __restrict__ moments,                         \
         float* __restrict__ second, OptArgs o, int num_workers,                           \
         const DevTile* __restrict__ pool, int32_t pool_count,                             \
-        unsigned long long* __restrict__ pool_counters, PoolBases pool_bases
+        unsigned long long* __restrict__ pool_counters, uint64_t pool_launch
 
 // Splits a tile's float4 index into a part folded into the base pointers
 // (a multiple of 2^20 float4, 16 MB) and a low part that keeps the per-lane
@@ -805,12 +805,16 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
                 (threadIdx.x >> 6) * (kStashTiles<S> * kStashTileVecs<S>) + (threadIdx.x & 63u);
     }
     if (pool_count > 0) {
-        // this workgroup's counter and the pool tiles it serves
-        const int nc = pool_bases.counters;
+        // this workgroup's counter, the pool tiles it serves, and the
+        // counter's value at the start of this launch
+        const int nc = pool_counter_count(gridDim.x);
         const int c = int(blockIdx.x % uint32_t(nc));
-        walk_pool<NW, OPT, PULL>(pool + c, int32_t(pool_counter_tiles(pool_count, c, nc)), nc,
-                                 pool_counters + c * kPoolCounterStride, pool_bases.base[c], grads,
-                                 outs, state, o, stash);
+        const int64_t served = pool_counter_tiles(pool_count, c, nc);
+        const uint64_t per_launch =
+            uint64_t(served) + uint64_t(kWavesPerBlock) * uint64_t(pool_counter_groups(gridDim.x, c, nc));
+        walk_pool<NW, OPT, PULL>(pool + c, int32_t(served), nc,
+                                 pool_counters + c * kPoolCounterStride,
+                                 pool_launch * per_launch, grads, outs, state, o, stash);
     } else {
         walk_tiles<NW, OPT, false, PULL>(tiles, tile_begin[bins + wave],
                                          tile_begin[bins + wave + 1], grads, outs, state, o, stash);
@@ -1060,7 +1064,7 @@ __global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS,
 
 #define PHUB_LAUNCH_ARGS                                                                     \
     p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.outs, p.weights, p.moments,        \
-        p.second, p.opt, p.num_workers, p.pool, p.pool_count, p.pool_counters, p.pool_bases
+        p.second, p.opt, p.num_workers, p.pool, p.pool_count, p.pool_counters, p.pool_launch
 
 template <int OPT, bool PULL>
 hipError_t launch_any(const StepParams& p, int grid, hipStream_t stream) {

@@ -105,19 +105,21 @@ inline void write_phase_ticks(int num_workers, int num_states, int64_t clock_khz
 }
 
 // Counters of the dynamic schedule.  The waves of workgroup g take from
-// counter g mod C (C = the launch's counters, at most kMaxPoolCounters and
-// at most its workgroups: one per XCD of MI355X, whose workgroups go to the
-// XCDs in turn), counter c serving pool tiles c, c + C, c + 2 C, ...  Each
-// counter sits on its own 256-byte line.  A counter is never reset: a launch
-// passes each counter's value at its start (base) and adds to it the tiles
-// it serves plus its waves (each wave takes once past its tiles).
+// counter g mod C (C = the launch's counters: kMaxPoolCounters, or fewer
+// for a grid of fewer workgroups; one per XCD of MI355X, whose workgroups
+// go to the XCDs in turn), counter c serving pool tiles c, c + C, c + 2 C,
+// ...  Each readiness group has its own counters, each on its own 256-byte
+// line, never reset: every launch of the group adds the same amount to
+// counter c (the tiles it serves plus the waves that take from it, each
+// wave taking once past its tiles), so the counter's value at the start of
+// the group's launch number L (from 0) is L times that amount.
 constexpr int kMaxPoolCounters = 8;
 constexpr int kPoolCounterStride = 32;  // unsigned long long: 256 bytes
 
-struct PoolBases {
-    uint64_t base[kMaxPoolCounters];
-    int32_t counters;  // C
-};
+// Counters a launch of `grid` workgroups uses.
+constexpr int pool_counter_count(int64_t grid) {
+    return grid < kMaxPoolCounters ? int(grid) : kMaxPoolCounters;
+}
 
 // Tiles of a pool of `count` tiles that counter c of C serves.
 constexpr int64_t pool_counter_tiles(int64_t count, int c, int counters) {
@@ -168,8 +170,8 @@ struct StepParams {
     // pool counters (see PoolCounters).  pool_count 0: none.
     const DevTile* pool;
     int32_t pool_count;
-    unsigned long long* pool_counters;  // kMaxPoolCounters counters, kPoolCounterStride apart
-    PoolBases pool_bases;
+    unsigned long long* pool_counters;  // the group's counters, kPoolCounterStride apart
+    uint64_t pool_launch;               // the group's launches before this one
 };
 
 // Whether the fused kernel for num_workers and optimizer (an OptKind) can

@@ -65,8 +65,7 @@ namespace {
 constexpr int kStageSlots = 4;       // pinned staging buffers for pointer-table uploads
 constexpr int kMaxWorkgroups = 1 << 16;  // largest persistent grid a job may ask for
 constexpr int64_t kArenaAlign = 64;  // elements: 256-byte aligned key slices
-constexpr size_t kCounterBytes =
-    size_t(phub::kMaxPoolCounters) * phub::kPoolCounterStride * sizeof(unsigned long long);
+constexpr size_t kCountersPerGroup = size_t(phub::kMaxPoolCounters) * phub::kPoolCounterStride;
 
 thread_local std::string g_error;
 
@@ -147,8 +146,8 @@ struct phub_job {
     int32_t* d_rem_begin = nullptr;   // same layout
     std::vector<int32_t> pool_begin;  // per readiness group: its tile pool in d_tiles
     std::vector<int32_t> pool_count;  // (0: the group's schedule is static)
-    unsigned long long* d_counters = nullptr;  // takes from the pools (never reset)
-    uint64_t counter_next[phub::kMaxPoolCounters] = {};  // their values when the next launch starts
+    unsigned long long* d_counters = nullptr;  // takes from the pools: per group, never reset
+    std::vector<uint64_t> pool_launches;        // per group: launches so far
     const float** d_grads = nullptr;  // [row * N + worker]
     float** d_outs = nullptr;         // same layout: pushpull model buffers
 
@@ -156,6 +155,10 @@ struct phub_job {
     std::vector<hipEvent_t> ready;    // same layout: event to wait for (none if null)
     bool ordered_events = false;      // each worker's events are ordered on one stream
     std::vector<hipEvent_t> group_last_event;  // [group * N + worker]: last event pushed this step
+    std::vector<int64_t> rgroup_events;  // pushes with a ready event this step, per group
+    int64_t step_events = 0;             // the same over all groups
+    int64_t step_outs = 0;               // model buffers registered this step
+    std::vector<hipEvent_t> wait_events; // reused by each launch: the events it waits for
     std::vector<uint8_t> pushed;      // same layout: pushed since the last step
     int64_t num_pushed = 0;
     std::vector<float*> outs;         // same layout: pushpull model buffers of this step
@@ -342,8 +345,11 @@ int launch_group(phub_job* j, int g) {
     // The events to wait for: every distinct one of the group's pushes, or
     // with ordered events each worker's last one; events already complete
     // need no wait.
-    std::vector<hipEvent_t> evs;
-    if (j->ordered_events) {
+    std::vector<hipEvent_t>& evs = j->wait_events;
+    evs.clear();
+    if (j->rgroup_events[g] == 0) {
+        // no push of this group came with an event
+    } else if (j->ordered_events) {
         for (size_t w = 0; w < n; ++w)
             if (hipEvent_t ev = j->group_last_event[size_t(g) * n + w]) evs.push_back(ev);
     } else {
@@ -375,22 +381,15 @@ int launch_group(phub_job* j, int g) {
         p.opt = optimizer_args(j);
         p.num_workers = j->num_workers;
         const int32_t pool = j->pool_count.empty() ? 0 : j->pool_count[g];
-        const int counters = std::min(phub::kMaxPoolCounters, j->groups);
         if (pool > 0) {
             p.pool = j->d_tiles + j->pool_begin[g];
             p.pool_count = pool;
-            p.pool_counters = j->d_counters;
-            p.pool_bases.counters = counters;
-            for (int c = 0; c < counters; ++c) p.pool_bases.base[c] = j->counter_next[c];
+            p.pool_counters = j->d_counters + size_t(g) * kCountersPerGroup;
+            p.pool_launch = j->pool_launches[g];
         }
         hipError_t e = phub::launch_fused_step(p, j->opt, j->groups, j->stream);
         if (e != hipSuccess) return hip_fail(e, "launch of the fused step kernel");
-        // each counter serves its tiles, and each of its waves takes once past them
-        if (pool > 0)
-            for (int c = 0; c < counters; ++c)
-                j->counter_next[c] += uint64_t(phub::pool_counter_tiles(pool, c, counters)) +
-                                      uint64_t(phub::kBlockThreads / 64) *
-                                          uint64_t(phub::pool_counter_groups(j->groups, c, counters));
+        if (pool > 0) ++j->pool_launches[g];
     }
     j->rgroup_launched[g] = 1;
     return PHUB_OK;
@@ -407,6 +406,7 @@ void record_out(phub_job* j, int worker, int key, float* out) {
     if (!j->has_out[i]) {
         j->has_out[i] = 1;
         ++j->rgroup_outs[g];
+        ++j->step_outs;
     }
 }
 
@@ -431,7 +431,11 @@ int record_push(phub_job* j, int worker, int key, const float* grad, hipEvent_t 
         j->rgroup_dirty[g] = 1;
     }
     j->ready[i] = ev;
-    if (ev && j->ordered_events) j->group_last_event[size_t(g) * j->num_workers + worker] = ev;
+    if (ev) {
+        ++j->rgroup_events[g];
+        ++j->step_events;
+        if (j->ordered_events) j->group_last_event[size_t(g) * j->num_workers + worker] = ev;
+    }
     if (!j->pushed[i]) {
         j->pushed[i] = 1;
         ++j->num_pushed;
@@ -554,6 +558,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
     float beta1 = 0, beta2 = 0, eps = 0;
     int workgroups = 0;  // 0: one per compute unit
     bool ordered_events = false;
+    bool whole_chunks = false;
     if (options) {
         if (options->workgroups < 0 || options->workgroups > kMaxWorkgroups)
             return fail(PHUB_EINVAL, "workgroups must be in [0, %d], got %d", kMaxWorkgroups,
@@ -597,6 +602,9 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         if (options->ordered_events != 0 && options->ordered_events != 1)
             return fail(PHUB_EINVAL, "ordered_events must be 0 or 1, got %d", options->ordered_events);
         ordered_events = options->ordered_events == 1;
+        if (options->whole_chunks != 0 && options->whole_chunks != 1)
+            return fail(PHUB_EINVAL, "whole_chunks must be 0 or 1, got %d", options->whole_chunks);
+        whole_chunks = options->whole_chunks == 1;
     }
 
     phub_job* j = new (std::nothrow) phub_job;
@@ -647,6 +655,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         }
         j->rgroup_work.assign(j->num_rgroups, 0);
         j->group_last_event.assign(size_t(j->num_rgroups) * num_workers, nullptr);
+        j->rgroup_events.assign(j->num_rgroups, 0);
         j->rgroup_pushed.assign(j->num_rgroups, 0);
         j->rgroup_launched.assign(j->num_rgroups, 0);
         j->rgroup_dirty.assign(j->num_rgroups, 1);
@@ -746,7 +755,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                                                chunk_bytes,
                                                schedule == PHUB_SCHEDULE_DYNAMIC ? phub::kScheduleLpt
                                                                                 : schedule,
-                                               bins, kLptItemsPerBin * bins, &plan);
+                                               bins, whole_chunks ? 0 : kLptItemsPerBin * bins,
+                                               &plan);
                     } else {
                         plan.bin_begin.assign(1, 0);
                     }
@@ -861,13 +871,16 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         const size_t tb_bytes = tile_begin.size() * sizeof(int32_t);
         const size_t rb_bytes = rem_begin.size() * sizeof(int32_t);
         const size_t tab_bytes = j->grads.size() * sizeof(const float*);
+        const size_t counter_bytes =
+            size_t(j->num_rgroups) * kCountersPerGroup * sizeof(unsigned long long);
+        j->pool_launches.assign(j->num_rgroups, 0);
         if (hipMalloc(&j->d_tiles, tile_bytes) != hipSuccess ||
             hipMalloc(&j->d_tile_begin, tb_bytes) != hipSuccess ||
             hipMalloc(&j->d_rems, rem_bytes) != hipSuccess ||
             hipMalloc(&j->d_rem_begin, rb_bytes) != hipSuccess ||
             hipMalloc(&j->d_grads, tab_bytes) != hipSuccess ||
             hipMalloc(&j->d_outs, tab_bytes) != hipSuccess ||
-            (j->dynamic && hipMalloc(&j->d_counters, kCounterBytes) != hipSuccess)) {
+            (j->dynamic && hipMalloc(&j->d_counters, counter_bytes) != hipSuccess)) {
             (void)hipGetLastError();
             rc = fail(PHUB_ENOMEM, "device allocation of the schedule failed");
             goto fail_cleanup;
@@ -883,7 +896,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         PHUB_TRY(hipMemcpy(j->d_tile_begin, tile_begin.data(), tb_bytes, hipMemcpyHostToDevice),
                  "hipMemcpy(tile bins)");
         if (j->d_counters)
-            PHUB_TRY(hipMemsetAsync(j->d_counters, 0, kCounterBytes, j->stream),
+            PHUB_TRY(hipMemsetAsync(j->d_counters, 0, counter_bytes, j->stream),
                      "hipMemsetAsync(pool counters)");
         PHUB_TRY(hipMemcpy(j->d_rem_begin, rem_begin.data(), rb_bytes, hipMemcpyHostToDevice),
                  "hipMemcpy(remainder bins)");
@@ -1032,12 +1045,19 @@ int phub_step(phub_job* j) {
         if (!j->rgroup_launched[g])
             if (int rc = launch_group(j, g)) return rc;
     std::fill(j->pushed.begin(), j->pushed.end(), 0);
-    std::fill(j->ready.begin(), j->ready.end(), nullptr);
-    std::fill(j->group_last_event.begin(), j->group_last_event.end(), nullptr);
+    if (j->step_events) {
+        std::fill(j->ready.begin(), j->ready.end(), nullptr);
+        std::fill(j->group_last_event.begin(), j->group_last_event.end(), nullptr);
+        std::fill(j->rgroup_events.begin(), j->rgroup_events.end(), 0);
+        j->step_events = 0;
+    }
     std::fill(j->rgroup_pushed.begin(), j->rgroup_pushed.end(), 0);
     std::fill(j->rgroup_launched.begin(), j->rgroup_launched.end(), 0);
-    std::fill(j->has_out.begin(), j->has_out.end(), 0);
-    std::fill(j->rgroup_outs.begin(), j->rgroup_outs.end(), 0);
+    if (j->step_outs) {
+        std::fill(j->has_out.begin(), j->has_out.end(), 0);
+        std::fill(j->rgroup_outs.begin(), j->rgroup_outs.end(), 0);
+        j->step_outs = 0;
+    }
     j->num_pushed = 0;
     ++j->steps_done;
     if (j->stage_claimed) {

@@ -58,7 +58,8 @@ class TorchJob:
                  resident_bytes: Optional[int] = None,
                  key_group: Optional[Sequence[int]] = None, unfused: bool = False,
                  optimizer: Optional[str] = None, betas=(0.9, 0.999), eps: float = 1e-8,
-                 workgroups: Optional[int] = None, ordered_events: bool = False):
+                 workgroups: Optional[int] = None, ordered_events: bool = False,
+                 whole_chunks: bool = False):
         import torch
         self.torch = torch
         self.spec = spec
@@ -77,13 +78,19 @@ class TorchJob:
                                              else _phub.OPTIMIZERS[optimizer],
                                              beta1=betas[0], beta2=betas[1], eps=eps,
                                              workgroups=workgroups,
-                                             ordered_events=int(bool(ordered_events)))
+                                             ordered_events=int(bool(ordered_events)),
+                                             whole_chunks=int(bool(whole_chunks)))
         self.optimizer = optimizer or "momentum"
         self.key_group = None if key_group is None else [int(g) for g in key_group]
         self._ptr_arrays: List = [None] * spec.num_workers
         self._grad_refs: List = [None] * spec.num_workers
         # every worker's key pointers in one table (worker-major) for phub_push_all
         self._all_ptrs = (ctypes.c_void_p * (spec.num_workers * spec.num_keys))()
+        self._attached = 0
+        # the two calls of every step, bound once (a step of a small job costs a
+        # few microseconds, and each layer of Python adds to it)
+        self._raw_push_all = self.lib.lib.phub_push_all
+        self._raw_step = self.lib.lib.phub_step
 
     # -- inputs ----------------------------------------------------------------
     def key_pointers(self, arena) -> List[int]:
@@ -95,6 +102,8 @@ class TorchJob:
         worker ``worker``'s gradients from now on."""
         if arena.numel() != self.arena_elems or arena.dtype != self.torch.float32:
             raise ValueError("gradient arena has the wrong size or dtype")
+        if self._grad_refs[worker] is None:
+            self._attached += 1
         self._grad_refs[worker] = arena
         ptrs = self.key_pointers(arena)
         self._ptr_arrays[worker] = _phub.pointer_array(ptrs)
@@ -114,10 +123,12 @@ class TorchJob:
     # -- the step --------------------------------------------------------------
     def push_all(self) -> None:
         """Every worker pushes every key from its attached arena (one call)."""
-        for w, arr in enumerate(self._ptr_arrays):
-            if arr is None:
-                raise RuntimeError(f"worker {w} has no gradient arena attached")
-        self.lib.phub_push_all(self.handle, self._all_ptrs)
+        if self._attached != self.spec.num_workers:
+            missing = [w for w, a in enumerate(self._ptr_arrays) if a is None]
+            raise RuntimeError(f"workers {missing} have no gradient arena attached")
+        rc = self._raw_push_all(self.handle, self._all_ptrs)
+        if rc:
+            self.lib._check(rc, True)
 
     def push_key(self, worker: int, key: int, event=None) -> None:
         """Push one key of worker ``worker`` from its attached arena; with
@@ -161,7 +172,9 @@ class TorchJob:
             self.lib.phub_pushpull_keys(self.handle, w, arr, self._model_ptrs[w])
 
     def step(self) -> None:
-        self.lib.phub_step(self.handle)
+        rc = self._raw_step(self.handle)
+        if rc:
+            self.lib._check(rc, True)
 
     def push_and_step(self) -> None:
         self.push_all()

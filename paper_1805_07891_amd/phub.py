@@ -61,7 +61,7 @@ class PhubOptions(ctypes.Structure):
                 ("num_groups", ctypes.c_int), ("key_group", ctypes.POINTER(ctypes.c_int)),
                 ("optimizer", ctypes.c_int), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("workgroups", ctypes.c_int), ("unfused", ctypes.c_int),
-                ("ordered_events", ctypes.c_int)]
+                ("ordered_events", ctypes.c_int), ("whole_chunks", ctypes.c_int)]
 
 
 class Library:
@@ -123,7 +123,7 @@ class Library:
                   key_group: Optional[Sequence[int]] = None, num_groups: Optional[int] = None,
                   unfused: bool = False, optimizer: Optional[int] = None, beta1: float = 0.9,
                   beta2: float = 0.999, eps: float = 1e-8, workgroups: Optional[int] = None,
-                  ordered_events: int = 0):
+                  ordered_events: int = 0, whole_chunks: int = 0):
         """Returns the job handle (an int), or (rc, None) with check=False on
         error.  With ``schedule``, ``resident_bytes`` or readiness groups
         (``key_group``: the group of each key; ``num_groups`` defaults to
@@ -135,7 +135,7 @@ class Library:
                 float(weight_decay), int(bool(nesterov)), hip_stream)
         if (schedule is None and resident_bytes is None and key_group is None and num_groups is None
                 and not unfused and optimizer is None and workgroups is None
-                and not ordered_events):
+                and not ordered_events and not whole_chunks):
             rc = self.lib.phub_init(*args)
         else:
             groups = None
@@ -150,7 +150,7 @@ class Library:
                                PHUB_OPT_MOMENTUM if optimizer is None else int(optimizer),
                                float(beta1), float(beta2), float(eps),
                                0 if workgroups is None else int(workgroups), int(bool(unfused)),
-                               int(ordered_events))
+                               int(ordered_events), int(whole_chunks))
             rc = self.lib.phub_init_ex(*args, ctypes.byref(opts))
         if rc != 0:
             self._check(rc, check)

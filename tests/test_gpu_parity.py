@@ -55,13 +55,14 @@ def _rel_err(x, ref):
 def run_small_case(torch, dev, lib, n_workers, key_elems, steps=2, chunk_bytes=32768,
                    lr=0.1, mu=0.9, wd=1e-4, nesterov=True, seed=0, push="keys",
                    reuse_buffers=False, stream=None, schedule=None, resident_bytes=None,
-                   unfused=False, workgroups=None):
+                   unfused=False, workgroups=None, whole_chunks=False):
     """Runs `steps` steps on the GPU and in the oracle; returns the job and
     per-step (gpu W, gpu M, oracle W, oracle M) lists per key."""
     spec = Job("case", n_workers, tuple(int(n) for n in key_elems), chunk_elems=chunk_bytes // 4,
                lr=lr, momentum=mu, weight_decay=wd, nesterov=nesterov, sigma_g=1e-2)
     job = TorchJob(spec, dev, stream=stream, chunk_bytes=chunk_bytes, lib=lib, schedule=schedule,
-                   resident_bytes=resident_bytes, unfused=unfused, workgroups=workgroups)
+                   resident_bytes=resident_bytes, unfused=unfused, workgroups=workgroups,
+                   whole_chunks=whole_chunks)
     offs, total = key_offsets(spec.key_elems)
     rng = np.random.default_rng(seed)
     w0 = np.zeros(total, np.float32)
@@ -165,13 +166,15 @@ def test_hyperparameter_corners(lib, torch_dev, hp):
         job.destroy()
 
 
-def test_chunk_size_does_not_change_results(lib, torch_dev):
+@pytest.mark.parametrize("whole_chunks", [False, True])
+def test_chunk_size_does_not_change_results(lib, torch_dev, whole_chunks):
     torch, dev = torch_dev
     keys = [3, 100, 8192 * 3 + 5, 70000, 1]
     outs = []
     for cb in (16, 48, 4096, 32768, 1 << 22):
-        _say("chunk bytes", cb)
-        job, res = run_small_case(torch, dev, lib, 6, keys, steps=2, chunk_bytes=cb, seed=99)
+        _say("chunk bytes", cb, "whole chunks", whole_chunks)
+        job, res = run_small_case(torch, dev, lib, 6, keys, steps=2, chunk_bytes=cb, seed=99,
+                                  whole_chunks=whole_chunks)
         assert_parity(res, f"chunk={cb}")
         outs.append(res[-1][:2])
         job.destroy()

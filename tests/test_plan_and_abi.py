@@ -248,11 +248,11 @@ def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
                dict(optimizer=2, beta1=1.0), dict(optimizer=2, beta2=-0.5),
                dict(optimizer=2, eps=-1.0), dict(optimizer=2, eps=float("inf")),
                dict(workgroups=-1), dict(workgroups=1 << 17), dict(key_elems=[4, 1 << 34]),
-               dict(ordered_events=2), dict(ordered_events=-1)]:
+               dict(ordered_events=2), dict(ordered_events=-1), dict(whole_chunks=2)]:
         a = dict(num_workers=2, key_elems=[4, 4], chunk_bytes=32768, lr=0.1, momentum=0.9,
                  weight_decay=1e-4, nesterov=True, schedule=None, resident_bytes=None,
                  key_group=None, num_groups=None, unfused=False, optimizer=None, beta1=0.9,
-                 beta2=0.999, eps=1e-8, workgroups=None, ordered_events=0)
+                 beta2=0.999, eps=1e-8, workgroups=None, ordered_events=0, whole_chunks=0)
         a.update(kw)
         rc, h = lib.phub_init(a["num_workers"], a["key_elems"], a["chunk_bytes"], a["lr"],
                               a["momentum"], a["weight_decay"], a["nesterov"], check=False,
@@ -260,7 +260,7 @@ def test_init_rejects_bad_arguments_before_touching_the_gpu(lib):
                               key_group=a["key_group"], num_groups=a["num_groups"],
                               unfused=a["unfused"], optimizer=a["optimizer"], beta1=a["beta1"],
                               beta2=a["beta2"], eps=a["eps"], workgroups=a["workgroups"],
-                              ordered_events=a["ordered_events"])
+                              ordered_events=a["ordered_events"], whole_chunks=a["whole_chunks"])
         assert rc == phub.PHUB_EINVAL and h is None, kw
 
 
