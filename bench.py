@@ -40,6 +40,8 @@ KERNEL_SOURCES = ["paper_1805_07891_amd/csrc/fused_step.hip", "paper_1805_07891_
                   "paper_1805_07891_amd/csrc/plan.cpp", "paper_1805_07891_amd/csrc/plan.hpp",
                   "paper_1805_07891_amd/csrc/phub_api.cpp"]
 HEADLINE_WORKLOAD = "multitenant"
+# The memory-side cache of MI355X, given to --pushpull jobs by default.
+PUSHPULL_CACHE_BYTES = 256 << 20
 
 
 def _code_only(text: str) -> str:
@@ -762,7 +764,12 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
         stream = streams[0] if shared_stream else streams[ji]
         if masked is not None:
             stream = masked[ji][0]
-        job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=args.resident_bytes,
+        # pushpull's kernels have no burst write-back: its jobs cache their
+        # state (256 MiB shared among the jobs) unless told otherwise
+        resident = args.resident_bytes
+        if resident is None and args.pushpull:
+            resident = PUSHPULL_CACHE_BYTES // len(wl.jobs)
+        job = TorchJob(spec, dev, stream=stream, lib=lib, resident_bytes=resident,
                        chunk_bytes=args.chunk_bytes, unfused=args.unfused,
                        optimizer=None if args.optimizer == "momentum" else args.optimizer,
                        schedule={"lpt": None, "split": PHUB_SCHEDULE_SPLIT,
