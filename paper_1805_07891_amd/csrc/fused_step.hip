@@ -354,19 +354,21 @@ constexpr int kPhases = kRing<NW, S, RES> / gcd_int(kTileLoads<NW, S>, kRing<NW,
 // state array (burst_write_back), the streamed bin does not write a piece's
 // new state as soon as it is computed: the state goes to a stash in LDS,
 // and the wave writes the stash back in one run of stores when it finishes
-// a tile inside the write window, or when the stash is full (kStashTiles
+// a piece inside the write window (then the tiles before the current one;
+// at a tile's end, the tile too), or when the stash is full (kStashTiles
 // tiles), or after its last tile.  The write window is the first part of a
 // period of the device's constant-rate wall clock, which every wave of
 // every launch on the chip reads alike: the waves write at the same time
 // and read at the same time, so HBM sees long runs of writes and long runs
 // of reads instead of a steady mix.  The period follows the tile's bytes
-// (kWritePeriodNsPerStream per stream: about the time a wave takes to fill
-// its stash) and the window is about two tiles long (kWriteWindowNs).
-// Measured on MI355X with nothing cached, fraction of peak (8 workers,
-// momentum): 143.7 M parameters 0.72 -> 0.80, 61.1 M 0.78 -> 0.80, 102 M
-// with 16 workers 0.77 -> 0.82; the same stash flushed only when full,
-// 0.73 on the first; flushed on each compute unit's own cycle counter
-// (not aligned across the chip) with the same period, 0.71.
+// (kWritePeriodNsPerStream per stream: about four tiles of a wave) and the
+// window is about one tile long (kWriteWindowNs).  Measured on MI355X with
+// nothing cached, fraction of peak (8 workers, momentum), piece by piece ->
+// burst write-back: 143.7 M parameters 0.72 -> 0.815, 61.1 M 0.78 -> 0.816,
+// 102 M with 16 workers 0.77 -> 0.84; the same stash flushed only when
+// full, 0.73 on the first; flushed on each compute unit's own cycle counter
+// (not aligned across the chip), 0.71; looked for only at the end of a tile
+// (with the best period and window for that), 1-2.6 points below.
 // Each lane reads back only the values it wrote, so the stash needs no
 // barrier, and results do not depend on when it is written back.  The
 // stash takes the compute unit's 160 KB of LDS (at most 40 KB per wave).
@@ -384,6 +386,24 @@ constexpr int kStashTileVecs = S * kVecPerLane * 64;
 template <int NW, int S, bool RES, bool PULL>
 constexpr bool kStash =
     !RES && !PULL && burst_write_back(NW, S) && kStashTiles<S> >= 2;
+
+// Where a wave's streamed bin stands in the burst write-back: tile t's
+// state goes to stash slot t mod kStashTiles, and tiles [t_stash, t) wait
+// in the stash.  `stash` is the lane's entry of the wave's first slot.
+struct StashCursor {
+    const DevTile* tiles;
+    PHUB_LDS f4* stash;
+    int32_t t;
+    int32_t t_stash;
+};
+
+#ifndef PHUB_PIECE_FLUSH
+#define PHUB_PIECE_FLUSH 1
+#endif
+// Whether a wave also looks for the write window after each piece of a
+// tile, not only at the end of the tile: the waves' write-backs then start
+// within a piece of the window's opening instead of within a tile.
+constexpr bool kPieceFlush = PHUB_PIECE_FLUSH != 0;
 
 template <int NW, int S, bool RES, int I>
 __device__ __forceinline__ f4 tile_load(const TileStreams<NW, S>& s) {
@@ -403,6 +423,39 @@ struct TilePipe {
     f4 sv[S][kVecPerLane];    // the state of each piece
 };
 
+// Whether the device's wall clock is inside a write window of the burst
+// write-back (the same answer for every lane: the clock is a scalar).  The
+// low 32 bits of the clock wrap every 43 s at 100 MHz; the wrap shifts the
+// phase of the periods once, which costs nothing but a slightly misplaced
+// window.
+__device__ __forceinline__ bool in_write_window(uint32_t period, uint32_t window) {
+    const uint32_t now = uint32_t(wall_clock64());
+    return now % period < window;
+}
+
+// Writes back the stashed state of the wave's tiles [t0, t1] (streamed
+// bin), tile by tile, each tile's S arrays piece by piece; tile t's state
+// is in stash slot t mod kStashTiles.  `stash` points at the lane's entry
+// of the wave's first stash slot.
+template <int NW, int S>
+__device__ __forceinline__ void write_stash(const DevTile* __restrict__ tiles, int32_t t0,
+                                            int32_t t1, const PHUB_LDS f4* stash,
+                                            float* const* state) {
+    for (int32_t t = t0; t <= t1; ++t) {
+        TileStreams<NW, S> s;
+        tile_bases<NW, S>(s, tiles[t], state);
+        const PHUB_LDS f4* ts = stash + (t % kStashTiles<S>) * kStashTileVecs<S>;
+#pragma unroll
+        for (int i = 0; i < S; ++i) {
+#pragma unroll
+            for (int u = 0; u < kVecPerLane; ++u) {
+                const f4 v = ts[(i * kVecPerLane + u) * 64];
+                store_wm<false>(s.st[i], s.off + u * 1024u, v);
+            }
+        }
+    }
+}
+
 // Step I of a tile: issue load I + kAhead (of this tile, or of the next one
 // if there is one), then consume load I.  After the last gradient of a
 // piece, that piece is optimized and written back.  Just before the first
@@ -415,7 +468,7 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
                                           TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
                                           uint64_t nrow, uint64_t prow, bool has_next,
                                           float* const* state, OptArgs o,
-                                          PHUB_LDS f4* tile_stash) {
+                                          PHUB_LDS f4* tile_stash, StashCursor* cur) {
     constexpr int S = kStates<OPT>;
     constexpr int L = kTileLoads<NW, S>;
     constexpr int R = kRing<NW, S, RES>;
@@ -449,6 +502,14 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
         if constexpr (kStash<NW, S, RES, PULL>) {
 #pragma unroll
             for (int i = 0; i < S; ++i) tile_stash[(i * kVecPerLane + u) * 64] = st[i];
+            // the window opened during this tile: write back the tiles
+            // before it now (this tile's pieces stay in its slot)
+            if constexpr (kPieceFlush && u + 1 < kVecPerLane) {
+                if (cur && cur->t != cur->t_stash && in_write_window(o.wb_period, o.wb_window)) {
+                    write_stash<NW, S>(cur->tiles, cur->t_stash, cur->t - 1, cur->stash, state);
+                    cur->t_stash = cur->t;
+                }
+            }
         } else {
 #pragma unroll
             for (int i = 0; i < S; ++i) store_wm<RES>(a.st[i], a.off + u * 1024u, st[i]);
@@ -471,41 +532,10 @@ __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>,
                                            TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
                                            uint64_t nrow, uint64_t prow, bool has_next,
                                            float* const* state, OptArgs o,
-                                           PHUB_LDS f4* tile_stash) {
-    (tile_step<NW, OPT, RES, PULL, PH, I>(p, a, b, nd, nrow, prow, has_next, state, o, tile_stash),
+                                           PHUB_LDS f4* tile_stash, StashCursor* cur) {
+    (tile_step<NW, OPT, RES, PULL, PH, I>(p, a, b, nd, nrow, prow, has_next, state, o, tile_stash,
+                                          cur),
      ...);
-}
-
-// Whether the device's wall clock is inside a write window of the burst
-// write-back (the same answer for every lane: the clock is a scalar).  The
-// low 32 bits of the clock wrap every 43 s at 100 MHz; the wrap shifts the
-// phase of the periods once, which costs nothing but a slightly misplaced
-// window.
-__device__ __forceinline__ bool in_write_window(uint32_t period, uint32_t window) {
-    const uint32_t now = uint32_t(wall_clock64());
-    return now % period < window;
-}
-
-// Writes back the stashed state of the wave's tiles [t0, t1] (streamed
-// bin), tile by tile, each tile's S arrays piece by piece.  `stash` points
-// at the lane's entry of the wave's first stash slot.
-template <int NW, int S>
-__device__ __forceinline__ void write_stash(const DevTile* __restrict__ tiles, int32_t t0,
-                                            int32_t t1, const PHUB_LDS f4* stash,
-                                            float* const* state) {
-    for (int32_t t = t0; t <= t1; ++t) {
-        TileStreams<NW, S> s;
-        tile_bases<NW, S>(s, tiles[t], state);
-        const PHUB_LDS f4* ts = stash + (t - t0) * kStashTileVecs<S>;
-#pragma unroll
-        for (int i = 0; i < S; ++i) {
-#pragma unroll
-            for (int u = 0; u < kVecPerLane; ++u) {
-                const f4 v = ts[(i * kVecPerLane + u) * 64];
-                store_wm<false>(s.st[i], s.off + u * 1024u, v);
-            }
-        }
-    }
 }
 
 template <int NW, int S, bool RES, int... I>
@@ -643,8 +673,8 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
     }
     DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
     tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
-    int32_t t_stash = tb;  // burst write-back: first tile whose state waits in the stash
-    int32_t t = tb;
+    StashCursor c{tiles, stash, tb, tb};  // c.t: the current tile
+    int32_t& t = c.t;
     // Tile t in ring phase PH; false after the bin's last tile.
     auto one_tile = [&](auto phase) -> bool {
         constexpr int PH = decltype(phase)::value;
@@ -654,14 +684,16 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
         if constexpr (PULL) nprow = load_row<NW>(outs + int64_t(nd.key) * NW);
         const DevTile nd2 = tiles[t + 2 <= last ? t + 2 : last];
         PHUB_LDS f4* tile_stash = nullptr;  // this tile's slot of the stash
-        if constexpr (kStash<NW, S, RES, PULL>) tile_stash = stash + (t - t_stash) * kStashTileVecs<S>;
+        if constexpr (kStash<NW, S, RES, PULL>)
+            tile_stash = stash + (t % kStashTiles<S>) * kStashTileVecs<S>;
         tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
-                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash);
+                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash,
+                                           &c);
         if constexpr (kStash<NW, S, RES, PULL>) {
-            if (t - t_stash == kStashTiles<S> - 1 || !has_next ||
+            if (t - c.t_stash == kStashTiles<S> - 1 || !has_next ||
                 in_write_window(o.wb_period, o.wb_window)) {
-                write_stash<NW, S>(tiles, t_stash, t, stash, state);
-                t_stash = t + 1;
+                write_stash<NW, S>(tiles, c.t_stash, t, stash, state);
+                c.t_stash = t + 1;
             }
         }
         if (!has_next) return false;
@@ -729,7 +761,8 @@ __device__ __forceinline__ void walk_pool(const DevTile* __restrict__ pool, int3
         PHUB_LDS f4* tile_stash = nullptr;  // this tile's slot of the stash
         if constexpr (STASH) tile_stash = stash + used * kStashTileVecs<S>;
         tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
-                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash);
+                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash,
+                                           nullptr);
         if constexpr (STASH) {
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k)

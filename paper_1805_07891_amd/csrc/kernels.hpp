@@ -88,9 +88,14 @@ constexpr bool burst_write_back(int num_workers, int num_states) {
 // into periods, and the first part of each period (the write window) is
 // when waves write back their stashed state.  Period per element stream of
 // a tile (N + 2 S streams: gradients, state read, state written) and
-// window, in nanoseconds; the host converts them to clock ticks.
-constexpr int64_t kWritePeriodNsPerStream = 3200;
-constexpr int64_t kWriteWindowNs = 15360;
+// window, in nanoseconds; the host converts them to clock ticks.  A
+// period is about four tiles of a wave's reads, so that the stash (five
+// tiles of momentum state, one of them the tile in progress) holds a
+// period's state; the window is about one tile.  Swept on MI355X with
+// 8 and 16 workers: 2200-2800 ns per stream and 6-10 us windows lie within
+// a point of each other, 3200 ns with a 15.4 us window 1-2.6 points below.
+constexpr int64_t kWritePeriodNsPerStream = 2600;
+constexpr int64_t kWriteWindowNs = 8000;
 
 // Write-phase period and window of the burst write-back in ticks of a wall
 // clock running at clock_khz, for a job with num_workers gradients and
