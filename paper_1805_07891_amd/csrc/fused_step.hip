@@ -604,44 +604,72 @@ __device__ __forceinline__ void write_stash_slots(const DevTile* __restrict__ po
 
 // The rest of a segment: nvec < 256 float4 then a ragged end of rem < 4
 // elements (one per lane).  stb: the S state bases, out: model buffers.
+// A remainder of a segment: nvec float4 and then rem (< 4) single elements
+// per array.  Every lane's loads of a group of up to kVecPerLane float4 per
+// array (as many as keep at most 64 loads in flight) and of its single
+// element are issued before the first is consumed: a remainder shorter
+// than a tile (the schedule's) costs one trip to memory, not one per
+// float4 of a lane.
 template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void partial(const float* const* g, float* const* stb,
                                         float* const* out, uint32_t nvec, uint32_t rem,
                                         OptArgs o) {
     constexpr int S = kStates<OPT>;
+    constexpr int kGroup = (NW + S) * kVecPerLane <= 64 ? kVecPerLane
+                           : 64 / (NW + S) > 0 ? 64 / (NW + S) : 1;
     const uint32_t lane = threadIdx.x & 63u;
-    for (uint32_t v = lane; v < nvec; v += 64u) {
-        f4 a[NW];
+    // the single elements of the last < 4, loaded with the first group
+    const int64_t ti = int64_t(nvec) * 4 + lane;
+    const bool tail = lane < rem;
+    float ta[NW], tst[S];
+    bool tail_loaded = false;
+    for (uint32_t v0 = 0; v0 < nvec || !tail_loaded; v0 += 64u * kGroup) {
+        f4 a[kGroup][NW];
+        f4 st[kGroup][S];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) a[w] = load_stream(g[w], v * 16u);
-        f4 st[S];
+        for (int j = 0; j < kGroup; ++j) {
+            const uint32_t v = v0 + 64u * j + lane;
+            if (v < nvec) {
 #pragma unroll
-        for (int i = 0; i < S; ++i) st[i] = load_wm<RES>(stb[i], v * 16u);
-        f4 s = a[0];
+                for (int w = 0; w < NW; ++w) a[j][w] = load_stream(g[w], v * 16u);
 #pragma unroll
-        for (int w = 1; w < NW; ++w) s = s + a[w];
-        update4<OPT>(s, st, o);
+                for (int i = 0; i < S; ++i) st[j][i] = load_wm<RES>(stb[i], v * 16u);
+            }
+        }
+        if (!tail_loaded && tail) {
 #pragma unroll
-        for (int i = 0; i < S; ++i) store_wm<RES>(stb[i], v * 16u, st[i]);
-        if constexpr (PULL) {
+            for (int w = 0; w < NW; ++w) ta[w] = load1(g[w], ti);
 #pragma unroll
-            for (int w = 0; w < NW; ++w) store_out(out[w], v * 16u, st[0]);
+            for (int k = 0; k < S; ++k) tst[k] = load1(stb[k], ti);
+        }
+        tail_loaded = true;
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) {
+            const uint32_t v = v0 + 64u * j + lane;
+            if (v < nvec) {
+                f4 s = a[j][0];
+#pragma unroll
+                for (int w = 1; w < NW; ++w) s = s + a[j][w];
+                update4<OPT>(s, st[j], o);
+#pragma unroll
+                for (int i = 0; i < S; ++i) store_wm<RES>(stb[i], v * 16u, st[j][i]);
+                if constexpr (PULL) {
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) store_out(out[w], v * 16u, st[j][0]);
+                }
+            }
         }
     }
-    if (lane < rem) {
-        const int64_t i = int64_t(nvec) * 4 + lane;
-        float s = load1(g[0], i);
+    if (tail) {
+        float s = ta[0];
 #pragma unroll
-        for (int w = 1; w < NW; ++w) s = s + load1(g[w], i);
-        float st[S];
+        for (int w = 1; w < NW; ++w) s = s + ta[w];
+        update<OPT>(s, tst, o);
 #pragma unroll
-        for (int k = 0; k < S; ++k) st[k] = load1(stb[k], i);
-        update<OPT>(s, st, o);
-#pragma unroll
-        for (int k = 0; k < S; ++k) store1(stb[k], i, st[k]);
+        for (int k = 0; k < S; ++k) store1(stb[k], ti, tst[k]);
         if constexpr (PULL) {
 #pragma unroll
-            for (int w = 0; w < NW; ++w) store1(out[w], i, st[0]);
+            for (int w = 0; w < NW; ++w) store1(out[w], ti, tst[0]);
         }
     }
 }
@@ -837,6 +865,12 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
         stash = (PHUB_LDS f4*)stash_lds +
                 (threadIdx.x >> 6) * (kStashTiles<S> * kStashTileVecs<S>) + (threadIdx.x & 63u);
     }
+    // the wave's four bins, all read at once (for a small job the trips to
+    // memory before the first data load are a good part of the launch)
+    const int32_t ts0 = tile_begin[bins + wave], ts1 = tile_begin[bins + wave + 1];
+    const int32_t tr0 = tile_begin[wave], tr1 = tile_begin[wave + 1];
+    const int32_t rr0 = rem_begin[wave], rr1 = rem_begin[wave + 1];
+    const int32_t rs0 = rem_begin[bins + wave], rs1 = rem_begin[bins + wave + 1];
     if (pool_count > 0) {
         // this workgroup's counter, the pool tiles it serves, and the
         // counter's value at the start of this launch
@@ -849,15 +883,11 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
                                  pool_counters + c * kPoolCounterStride,
                                  pool_launch * per_launch, grads, outs, state, o, stash);
     } else {
-        walk_tiles<NW, OPT, false, PULL>(tiles, tile_begin[bins + wave],
-                                         tile_begin[bins + wave + 1], grads, outs, state, o, stash);
+        walk_tiles<NW, OPT, false, PULL>(tiles, ts0, ts1, grads, outs, state, o, stash);
     }
-    walk_tiles<NW, OPT, true, PULL>(tiles, tile_begin[wave], tile_begin[wave + 1], grads, outs,
-                                    state, o, stash);
-    walk_rems<NW, OPT, true, PULL>(rems, rem_begin[wave], rem_begin[wave + 1], grads, outs, state,
-                                   o);
-    walk_rems<NW, OPT, false, PULL>(rems, rem_begin[bins + wave], rem_begin[bins + wave + 1], grads,
-                                    outs, state, o);
+    walk_tiles<NW, OPT, true, PULL>(tiles, tr0, tr1, grads, outs, state, o, stash);
+    walk_rems<NW, OPT, true, PULL>(rems, rr0, rr1, grads, outs, state, o);
+    walk_rems<NW, OPT, false, PULL>(rems, rs0, rs1, grads, outs, state, o);
 }
 
 // Any N: workers taken in batches of kBatch, each batch's loads in flight
