@@ -361,8 +361,9 @@ constexpr int kPhases = kRing<NW, S, RES> / gcd_int(kTileLoads<NW, S>, kRing<NW,
 // every launch on the chip reads alike: the waves write at the same time
 // and read at the same time, so HBM sees long runs of writes and long runs
 // of reads instead of a steady mix.  The period follows the tile's bytes
-// (kWritePeriodNsPerStream per stream: about four tiles of a wave) and the
-// window is about one tile long (kWriteWindowNs).  Measured on MI355X with
+// and the stash's size (kWritePeriodNsPerStreamTile: about as many tiles of
+// a wave as the stash holds besides the one in progress) and the window is
+// about one tile long (kWriteWindowNs).  Measured on MI355X with
 // nothing cached, fraction of peak (8 workers, momentum), piece by piece ->
 // burst write-back: 143.7 M parameters 0.72 -> 0.815, 61.1 M 0.78 -> 0.816,
 // 102 M with 16 workers 0.77 -> 0.84; the same stash flushed only when
@@ -373,11 +374,11 @@ constexpr int kPhases = kRing<NW, S, RES> / gcd_int(kTileLoads<NW, S>, kRing<NW,
 // barrier, and results do not depend on when it is written back.  The
 // stash takes the compute unit's 160 KB of LDS (at most 40 KB per wave).
 constexpr int kLdsBytes = 160 * 1024;
-constexpr int kStashBytesPerWave =
-    kLdsBytes / kWavesPerBlock < 40 * 1024 ? kLdsBytes / kWavesPerBlock : 40 * 1024;
+static_assert(kStashBytesPerWave * kWavesPerBlock <= kLdsBytes, "the stash fits the LDS");
 
 template <int S>
-constexpr int kStashTiles = kStashBytesPerWave / (S * kVecPerLane * 1024);
+constexpr int kStashTiles = stash_tiles(S);
+static_assert(kVecPerLane * 1024 == 4 * 1024, "a tile is 4 KB per array and wave");
 
 // float4 per tile and per wave in the stash (lane l holds entry l of every 64)
 template <int S>
@@ -387,23 +388,6 @@ template <int NW, int S, bool RES, bool PULL>
 constexpr bool kStash =
     !RES && !PULL && burst_write_back(NW, S) && kStashTiles<S> >= 2;
 
-// Where a wave's streamed bin stands in the burst write-back: tile t's
-// state goes to stash slot t mod kStashTiles, and tiles [t_stash, t) wait
-// in the stash.  `stash` is the lane's entry of the wave's first slot.
-struct StashCursor {
-    const DevTile* tiles;
-    PHUB_LDS f4* stash;
-    int32_t t;
-    int32_t t_stash;
-};
-
-#ifndef PHUB_PIECE_FLUSH
-#define PHUB_PIECE_FLUSH 1
-#endif
-// Whether a wave also looks for the write window after each piece of a
-// tile, not only at the end of the tile: the waves' write-backs then start
-// within a piece of the window's opening instead of within a tile.
-constexpr bool kPieceFlush = PHUB_PIECE_FLUSH != 0;
 
 template <int NW, int S, bool RES, int I>
 __device__ __forceinline__ f4 tile_load(const TileStreams<NW, S>& s) {
@@ -456,19 +440,36 @@ __device__ __forceinline__ void write_stash(const DevTile* __restrict__ tiles, i
     }
 }
 
+// Where a wave's walk over a list of tiles stands in the burst write-back:
+// tile t's state goes to stash slot t mod kStashTiles, and the tiles
+// [t_stash, t) before the current one t wait in the stash.
+struct TileCursor {
+    const DevTile* tiles;
+    PHUB_LDS f4* stash;  // the lane's entry of the wave's first slot
+    int32_t t;
+    int32_t t_stash;
+    __device__ bool waiting() const { return t != t_stash; }
+    // write back the tiles before the current one
+    template <int NW, int S>
+    __device__ void write_back_before(float* const* state) {
+        write_stash<NW, S>(tiles, t_stash, t - 1, stash, state);
+        t_stash = t;
+    }
+};
+
 // Step I of a tile: issue load I + kAhead (of this tile, or of the next one
 // if there is one), then consume load I.  After the last gradient of a
 // piece, that piece is optimized and written back.  Just before the first
 // load of the next tile is issued, the next tile's streams are formed from
 // its descriptor and pointer row, which were fetched at the start of this
 // tile.
-template <int NW, int OPT, bool RES, bool PULL, int PH, int I>
+template <int NW, int OPT, bool RES, bool PULL, int PH, int I, typename Cursor>
 __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
                                           const TileStreams<NW, kStates<OPT>>& a,
                                           TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
                                           uint64_t nrow, uint64_t prow, bool has_next,
                                           float* const* state, OptArgs o,
-                                          PHUB_LDS f4* tile_stash, StashCursor* cur) {
+                                          PHUB_LDS f4* tile_stash, Cursor* cur) {
     constexpr int S = kStates<OPT>;
     constexpr int L = kTileLoads<NW, S>;
     constexpr int R = kRing<NW, S, RES>;
@@ -503,12 +504,12 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
 #pragma unroll
             for (int i = 0; i < S; ++i) tile_stash[(i * kVecPerLane + u) * 64] = st[i];
             // the window opened during this tile: write back the tiles
-            // before it now (this tile's pieces stay in its slot)
-            if constexpr (kPieceFlush && u + 1 < kVecPerLane) {
-                if (cur && cur->t != cur->t_stash && in_write_window(o.wb_period, o.wb_window)) {
-                    write_stash<NW, S>(cur->tiles, cur->t_stash, cur->t - 1, cur->stash, state);
-                    cur->t_stash = cur->t;
-                }
+            // before it now (this tile's pieces stay in its slot), so that
+            // the waves' write-backs start within a piece of the window's
+            // opening instead of within a tile
+            if constexpr (u + 1 < kVecPerLane) {
+                if (cur->waiting() && in_write_window(o.wb_period, o.wb_window))
+                    cur->template write_back_before<NW, S>(state);
             }
         } else {
 #pragma unroll
@@ -525,14 +526,14 @@ __device__ __forceinline__ void tile_step(TilePipe<NW, kStates<OPT>, RES>& p,
     __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int NW, int OPT, bool RES, bool PULL, int PH, int... I>
+template <int NW, int OPT, bool RES, bool PULL, int PH, typename Cursor, int... I>
 __device__ __forceinline__ void tile_steps(std::integer_sequence<int, I...>,
                                            TilePipe<NW, kStates<OPT>, RES>& p,
                                            const TileStreams<NW, kStates<OPT>>& a,
                                            TileStreams<NW, kStates<OPT>>& b, const DevTile& nd,
                                            uint64_t nrow, uint64_t prow, bool has_next,
                                            float* const* state, OptArgs o,
-                                           PHUB_LDS f4* tile_stash, StashCursor* cur) {
+                                           PHUB_LDS f4* tile_stash, Cursor* cur) {
     (tile_step<NW, OPT, RES, PULL, PH, I>(p, a, b, nd, nrow, prow, has_next, state, o, tile_stash,
                                           cur),
      ...);
@@ -578,13 +579,17 @@ __device__ __forceinline__ int32_t resolve_take(uint64_t v, uint64_t base, int32
 // Writes back the stashed state of the first `used` stash slots, slot i
 // holding pool tile pool[idx[i] * stride] (burst write-back of the pool
 // walk).
+// Writes back the `count` stashed tiles of a pool walk whose oldest sits in
+// stash slot `first`, the next ones in the slots after it (mod SLOTS);
+// slot k holds pool tile pool[idx[k] * stride].
 template <int NW, int S, int SLOTS>
 __device__ __forceinline__ void write_stash_slots(const DevTile* __restrict__ pool, int stride,
-                                                  const int32_t (&idx)[SLOTS], int used,
-                                                  const PHUB_LDS f4* stash, float* const* state) {
+                                                  const int32_t (&idx)[SLOTS], int first,
+                                                  int count, const PHUB_LDS f4* stash,
+                                                  float* const* state) {
 #pragma unroll
     for (int k = 0; k < SLOTS; ++k) {
-        if (k < used) {
+        if ((k - first + SLOTS) % SLOTS < count) {
             TileStreams<NW, S> s;
             tile_bases<NW, S>(s, pool[int64_t(idx[k]) * stride], state);
             const PHUB_LDS f4* ts = stash + k * kStashTileVecs<S>;
@@ -600,10 +605,33 @@ __device__ __forceinline__ void write_stash_slots(const DevTile* __restrict__ po
     }
 }
 
+// Where a wave's pool walk stands in the burst write-back: its n-th tile
+// (counted from 0) goes to stash slot n mod SLOTS, and the tiles
+// [first, n) before the current one wait in the stash.
+template <int SLOTS>
+struct PoolCursor {
+    const DevTile* pool;
+    int stride;
+    PHUB_LDS f4* stash;
+    int32_t idx[SLOTS];  // the pool tile held by each slot
+    int32_t n;
+    int32_t first;
+    __device__ bool waiting() const { return n != first; }
+    // write back the tiles [first, end)
+    template <int NW, int S>
+    __device__ void write_back_to(int32_t end, float* const* state) {
+        write_stash_slots<NW, S, SLOTS>(pool, stride, idx, first % SLOTS, end - first, stash,
+                                        state);
+        first = end;
+    }
+    template <int NW, int S>
+    __device__ void write_back_before(float* const* state) {
+        write_back_to<NW, S>(n, state);
+    }
+};
+
 // ------------------------------------------------------------ remainders
 
-// The rest of a segment: nvec < 256 float4 then a ragged end of rem < 4
-// elements (one per lane).  stb: the S state bases, out: model buffers.
 // A remainder of a segment: nvec float4 and then rem (< 4) single elements
 // per array.  Every lane's loads of a group of up to kVecPerLane float4 per
 // array (as many as keep at most 64 loads in flight) and of its single
@@ -701,7 +729,7 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
     }
     DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
     tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
-    StashCursor c{tiles, stash, tb, tb};  // c.t: the current tile
+    TileCursor c{tiles, stash, tb, tb};  // c.t: the current tile
     int32_t& t = c.t;
     // Tile t in ring phase PH; false after the bin's last tile.
     auto one_tile = [&](auto phase) -> bool {
@@ -774,8 +802,7 @@ __device__ __forceinline__ void walk_pool(const DevTile* __restrict__ pool, int3
     }
     DevTile nd = pool[int64_t(n1 >= 0 ? n1 : cur) * stride];
     tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
-    int32_t slot[SLOTS];  // burst write-back: pool tiles whose state waits in the stash
-    int used = 0;
+    PoolCursor<SLOTS> c{pool, stride, stash, {}, 0, 0};  // burst write-back
     auto one_tile = [&](auto phase) -> bool {
         constexpr int PH = decltype(phase)::value;
         const bool has_next = n1 >= 0;
@@ -787,19 +814,20 @@ __device__ __forceinline__ void walk_pool(const DevTile* __restrict__ pool, int3
         const uint64_t v3 = take3 ? issue_take(counter) : 0;
         const DevTile nd2 = pool[int64_t(n2 >= 0 ? n2 : cur) * stride];
         PHUB_LDS f4* tile_stash = nullptr;  // this tile's slot of the stash
-        if constexpr (STASH) tile_stash = stash + used * kStashTileVecs<S>;
-        tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
-                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash,
-                                           nullptr);
         if constexpr (STASH) {
+            const int sl = c.n % SLOTS;
+            tile_stash = stash + sl * kStashTileVecs<S>;
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k)
-                if (k == used) slot[k] = cur;
-            ++used;
-            if (used == SLOTS || !has_next || in_write_window(o.wb_period, o.wb_window)) {
-                write_stash_slots<NW, S, SLOTS>(pool, stride, slot, used, stash, state);
-                used = 0;
-            }
+                if (k == sl) c.idx[k] = cur;
+        }
+        tile_steps<NW, OPT, RES, PULL, PH>(std::make_integer_sequence<int, kTileLoads<NW, S>>{}, p,
+                                           a, b, nd, nrow, prow, has_next, state, o, tile_stash,
+                                           &c);
+        if constexpr (STASH) {
+            ++c.n;
+            if (c.n - c.first == SLOTS || !has_next || in_write_window(o.wb_period, o.wb_window))
+                c.template write_back_to<NW, S>(c.n, state);
         }
         if (!has_next) return false;
         a = b;

@@ -83,18 +83,29 @@ constexpr bool burst_write_back(int num_workers, int num_states) {
            num_workers >= kBurstMinWorkers[num_states - 1];
 }
 
+// The burst write-back's stash: LDS per wave (the compute unit's 160 KB
+// over its four waves), and how many tiles of state it holds for a job
+// with num_states state arrays (a tile is 4 KB per array and wave).
+constexpr int kStashBytesPerWave = 40 * 1024;
+constexpr int stash_tiles(int num_states) {
+    return num_states >= 1 ? kStashBytesPerWave / (num_states * 4 * 1024) : 0;
+}
+
 // Chip-wide write phases of the burst write-back.  Every wave of every
 // launch reads the same constant-rate wall clock; the clock's time is cut
 // into periods, and the first part of each period (the write window) is
-// when waves write back their stashed state.  Period per element stream of
-// a tile (N + 2 S streams: gradients, state read, state written) and
-// window, in nanoseconds; the host converts them to clock ticks.  A
-// period is about four tiles of a wave's reads, so that the stash (five
-// tiles of momentum state, one of them the tile in progress) holds a
-// period's state; the window is about one tile.  Swept on MI355X with
-// 8 and 16 workers: 2200-2800 ns per stream and 6-10 us windows lie within
-// a point of each other, 3200 ns with a 15.4 us window 1-2.6 points below.
-constexpr int64_t kWritePeriodNsPerStream = 2600;
+// when waves write back their stashed state.  A period is about as many
+// tiles of a wave's reads as the stash holds besides the tile in progress
+// (4 of momentum's 5, 9 of plain SGD's 10, 2 of Adam's 3), at
+// kWritePeriodNsPerStreamTile per element stream of a tile (N + 2 S
+// streams: gradients, state read, state written) and stashed tile; the
+// window is about one tile (kWriteWindowNs).  The host converts both to
+// clock ticks.  Swept on MI355X with momentum at 8 and 16 workers: 550-700
+// ns per stream and tile and 6-10 us windows lie within a point of each
+// other, 800 ns with a 15.4 us window 1-2.6 points below; a period of
+// four tiles for every optimizer measured 1.5-2.7 points below this for
+// plain SGD at 8 workers and 1.8 below for Adam at 16.
+constexpr int64_t kWritePeriodNsPerStreamTile = 650;
 constexpr int64_t kWriteWindowNs = 8000;
 
 // Write-phase period and window of the burst write-back in ticks of a wall
@@ -103,7 +114,8 @@ constexpr int64_t kWriteWindowNs = 8000;
 inline void write_phase_ticks(int num_workers, int num_states, int64_t clock_khz,
                               uint32_t* period, uint32_t* window) {
     const int64_t streams = num_workers + 2 * int64_t(num_states);
-    const int64_t p = kWritePeriodNsPerStream * streams * clock_khz / 1000000;
+    const int64_t tiles = std::max<int64_t>(stash_tiles(num_states) - 1, 1);
+    const int64_t p = kWritePeriodNsPerStreamTile * streams * tiles * clock_khz / 1000000;
     const int64_t w = kWriteWindowNs * clock_khz / 1000000;
     *period = uint32_t(std::min<int64_t>(std::max<int64_t>(p, 2), INT32_MAX));
     *window = uint32_t(std::min<int64_t>(std::max<int64_t>(w, 1), *period - 1));
@@ -144,7 +156,7 @@ struct OptArgs {
     float mu;
     float wd;
     float b1, b2, c1, c2, k1, k2, eps;
-    // burst write-back (see kWritePeriodNsPerStream): the write phases'
+    // burst write-back (see kWritePeriodNsPerStreamTile): the write phases'
     // period and window in ticks of the device's wall clock
     uint32_t wb_period;
     uint32_t wb_window;
