@@ -576,9 +576,6 @@ __device__ __forceinline__ int32_t resolve_take(uint64_t v, uint64_t base, int32
     return i >= 0 && i < int64_t(count) ? int32_t(i) : -1;
 }
 
-// Writes back the stashed state of the first `used` stash slots, slot i
-// holding pool tile pool[idx[i] * stride] (burst write-back of the pool
-// walk).
 // Writes back the `count` stashed tiles of a pool walk whose oldest sits in
 // stash slot `first`, the next ones in the slots after it (mod SLOTS);
 // slot k holds pool tile pool[idx[k] * stride].
