@@ -677,6 +677,23 @@ _OWN_FLAGS = {"--workload": 1, "--cpu-seconds": 1, "--config-cpu-seconds": 1, "-
 CONFIG_MIN_TIMED_MS = 50.0
 
 
+def child_args(argv) -> list:
+    """The command-line arguments a workload's process gets from the parent:
+    all but the flags the parent handles itself (with their values, given
+    as `--flag value` or `--flag=value`)."""
+    passed = []
+    i = 0
+    while i < len(argv):
+        a = argv[i]
+        flag = a.split("=", 1)[0]
+        if flag in _OWN_FLAGS:
+            i += 1 if "=" in a else 1 + _OWN_FLAGS[flag]
+            continue
+        passed.append(a)
+        i += 1
+    return passed
+
+
 def run_all(args, argv) -> int:
     """The five workloads, each measured by this script in a process of its
     own (this process never touches the GPU).  Measured in one process one
@@ -690,16 +707,7 @@ def run_all(args, argv) -> int:
     "configs"."""
     import subprocess
     from paper_1805_07891_amd import workloads
-    passed = []
-    i = 0
-    while i < len(argv):
-        a = argv[i]
-        flag = a.split("=", 1)[0]
-        if flag in _OWN_FLAGS:
-            i += 1 if "=" in a else 1 + _OWN_FLAGS[flag]
-            continue
-        passed.append(a)
-        i += 1
+    passed = child_args(argv)
     lines = {}
     for name in workloads.WORKLOAD_NAMES:
         budget = args.cpu_seconds if name == HEADLINE_WORKLOAD else args.config_cpu_seconds
