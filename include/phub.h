@@ -393,7 +393,7 @@ int phub_destroy(phub_job *job);
  *                 stream).
  * The step's schedule and pointer table live in a device array of the
  * library of 4 MiB (PHUB_NOALLOC_SCRATCH_BYTES), one per GPU, held until
- * the process ends; that bounds a call to about 250 M parameters and
+ * the process ends; that bounds a call to about 240 M parameters and
  * PHUB_EINVAL reports a step that does not fit, before anything is
  * enqueued.  The call uploads the schedule on hip_stream after the stream's
  * earlier work and waits for that upload (the host thread blocks until the

@@ -203,6 +203,7 @@ __device__ __forceinline__ uint32_t wave_index() {
 #define PHUB_KERNEL_ARGS                                                                  \
     const DevTile* __restrict__ tiles, const int32_t* __restrict__ tile_begin,            \
         const DevRem* __restrict__ rems, const int32_t* __restrict__ rem_begin,           \
+        const WaveHead* __restrict__ heads,                                               \
         const float* const* __restrict__ grads, float* const* __restrict__ outs,          \
         float* __restrict__ weights, float* __restrict__ moments,                         \
         float* __restrict__ second, OptArgs o, int num_workers,                           \
@@ -701,14 +702,16 @@ __device__ __forceinline__ void partial(const float* const* g, float* const* stb
 
 // ---------------------------------------------------------------- kernels
 
-// The full tiles [tb, te) of one bin, NW workers, state policy RES.  At
+// The full tiles [tb, te) of one bin, NW workers, state policy RES; `first`
+// is tiles[tb], which the wave has from its head.  At
 // the start of tile t the wave fetches the pointer row of tile t + 1 (one
 // vector load), whose descriptor it fetched at the start of tile t - 1, and
 // the descriptor of tile t + 2 (a scalar load); both have long arrived when
 // the window reaches tile t + 1.
 template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, int32_t tb,
-                                           int32_t te, const float* const* __restrict__ grads,
+                                           int32_t te, const DevTile& first,
+                                           const float* const* __restrict__ grads,
                                            float* const* __restrict__ outs, float* const* state,
                                            OptArgs o, PHUB_LDS f4* stash) {
     constexpr int S = kStates<OPT>;
@@ -719,11 +722,8 @@ __device__ __forceinline__ void walk_tiles(const DevTile* __restrict__ tiles, in
     TilePipe<NW, S, RES> p;
     TileStreams<NW, S> a, b;
     uint64_t prow = 0;  // pushpull: model-buffer pointer row of the current tile
-    {
-        const DevTile first = tiles[tb];
-        tile_streams<NW, S>(a, first, grads + int64_t(first.key) * NW, state);
-        if constexpr (PULL) prow = load_row<NW>(outs + int64_t(first.key) * NW);
-    }
+    tile_streams<NW, S>(a, first, grads + int64_t(first.key) * NW, state);
+    if constexpr (PULL) prow = load_row<NW>(outs + int64_t(first.key) * NW);
     DevTile nd = tiles[tb + 1 <= last ? tb + 1 : last];
     tile_prologue<NW, S, RES>(std::make_integer_sequence<int, kAhead<NW, S, RES>>{}, p, a);
     TileCursor c{tiles, stash, tb, tb};  // c.t: the current tile
@@ -845,15 +845,19 @@ __device__ __forceinline__ void walk_pool(const DevTile* __restrict__ pool, int3
     }
 }
 
-// The remainders [rb, re) of one bin.
+// The remainders [rb, re) of one bin; `first` is rems[rb], which the wave
+// has from its head.  The descriptor of the next remainder is fetched while
+// this one is processed.
 template <int NW, int OPT, bool RES, bool PULL>
 __device__ __forceinline__ void walk_rems(const DevRem* __restrict__ rems, int32_t rb, int32_t re,
+                                          const DevRem& first,
                                           const float* const* __restrict__ grads,
                                           float* const* __restrict__ outs, float* const* state,
                                           OptArgs o) {
     constexpr int S = kStates<OPT>;
+    DevRem rm = first;
     for (int32_t r = rb; r < re; ++r) {
-        const DevRem rm = rems[r];
+        const DevRem next = rems[r + 1 < re ? r + 1 : r];
         const float* g[NW];
         float* out[NW];
 #pragma unroll
@@ -866,6 +870,7 @@ __device__ __forceinline__ void walk_rems(const DevRem* __restrict__ rems, int32
         for (int i = 0; i < S; ++i) stb[i] = state[i] + rm.arena_offset;
         partial<NW, OPT, RES, PULL>(g, stb, out, uint32_t(rm.count) >> 2,
                                     uint32_t(rm.count) & 3u, o);
+        rm = next;
     }
 }
 
@@ -882,7 +887,6 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
     PHUB_KERNEL_ARGS) {
     float* const state[3] = {weights, moments, second};
     const uint32_t wave = wave_index();
-    const uint32_t bins = gridDim.x * kWavesPerBlock;
     constexpr int S = kStates<OPT>;
     PHUB_LDS f4* stash = nullptr;  // the lane's entry of its wave's stash
     if constexpr (kStash<NW, S, false, PULL>) {
@@ -890,12 +894,8 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
         stash = (PHUB_LDS f4*)stash_lds +
                 (threadIdx.x >> 6) * (kStashTiles<S> * kStashTileVecs<S>) + (threadIdx.x & 63u);
     }
-    // the wave's four bins, all read at once (for a small job the trips to
-    // memory before the first data load are a good part of the launch)
-    const int32_t ts0 = tile_begin[bins + wave], ts1 = tile_begin[bins + wave + 1];
-    const int32_t tr0 = tile_begin[wave], tr1 = tile_begin[wave + 1];
-    const int32_t rr0 = rem_begin[wave], rr1 = rem_begin[wave + 1];
-    const int32_t rs0 = rem_begin[bins + wave], rs1 = rem_begin[bins + wave + 1];
+    // the wave's bins and the first descriptor of each, read at once
+    const WaveHead h = heads[wave];
     if (pool_count > 0) {
         // this workgroup's counter, the pool tiles it serves, and the
         // counter's value at the start of this launch
@@ -908,11 +908,15 @@ __global__ __launch_bounds__(kBlockThreads) PHUB_ONE_WAVE_PER_SIMD void fused_st
                                  pool_counters + c * kPoolCounterStride,
                                  pool_launch * per_launch, grads, outs, state, o, stash);
     } else {
-        walk_tiles<NW, OPT, false, PULL>(tiles, ts0, ts1, grads, outs, state, o, stash);
+        walk_tiles<NW, OPT, false, PULL>(tiles, h.tiles_streamed[0], h.tiles_streamed[1],
+                                         h.first_streamed, grads, outs, state, o, stash);
     }
-    walk_tiles<NW, OPT, true, PULL>(tiles, tr0, tr1, grads, outs, state, o, stash);
-    walk_rems<NW, OPT, true, PULL>(rems, rr0, rr1, grads, outs, state, o);
-    walk_rems<NW, OPT, false, PULL>(rems, rs0, rs1, grads, outs, state, o);
+    walk_tiles<NW, OPT, true, PULL>(tiles, h.tiles_resident[0], h.tiles_resident[1],
+                                    h.first_resident, grads, outs, state, o, stash);
+    walk_rems<NW, OPT, true, PULL>(rems, h.rems_resident[0], h.rems_resident[1],
+                                   h.first_rem_resident, grads, outs, state, o);
+    walk_rems<NW, OPT, false, PULL>(rems, h.rems_streamed[0], h.rems_streamed[1],
+                                    h.first_rem_streamed, grads, outs, state, o);
 }
 
 // Any N: workers taken in batches of kBatch, each batch's loads in flight
@@ -1151,7 +1155,8 @@ __global__ __launch_bounds__(kBlockThreads) void optimize_only(PHUB_KERNEL_ARGS,
 // -------------------------------------------------------------- launchers
 
 #define PHUB_LAUNCH_ARGS                                                                     \
-    p.tiles, p.tile_begin, p.rems, p.rem_begin, p.grads, p.outs, p.weights, p.moments,        \
+    p.tiles, p.tile_begin, p.rems, p.rem_begin, p.heads, p.grads, p.outs, p.weights,         \
+        p.moments,                                                                           \
         p.second, p.opt, p.num_workers, p.pool, p.pool_count, p.pool_counters, p.pool_launch
 
 template <int OPT, bool PULL>
@@ -1269,6 +1274,7 @@ bool takes_tile_pool(int num_workers, int optimizer) {
 hipError_t launch_fused_step(const StepParams& p, int optimizer, int grid, hipStream_t stream) {
     if (p.pool_count > 0 && (p.merge || !takes_tile_pool(p.num_workers, optimizer)))
         return hipErrorInvalidValue;  // only the fixed-N fused kernels walk a pool
+    if (!p.merge && !p.heads) return hipErrorInvalidValue;  // the fixed-N kernels read them
     switch (optimizer) {
         case kOptMomentum: return launch_opt<kOptMomentum>(p, grid, stream);
         case kOptNesterov: return launch_opt<kOptNesterov>(p, grid, stream);

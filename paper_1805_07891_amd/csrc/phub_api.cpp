@@ -144,6 +144,7 @@ struct phub_job {
     int32_t* d_tile_begin = nullptr;  // num_rgroups blocks of 2 * bins + 1 entries
     phub::DevRem* d_rems = nullptr;
     int32_t* d_rem_begin = nullptr;   // same layout
+    phub::WaveHead* d_heads = nullptr;  // num_rgroups blocks of bins heads
     std::vector<int32_t> pool_begin;  // per readiness group: its tile pool in d_tiles
     std::vector<int32_t> pool_count;  // (0: the group's schedule is static)
     unsigned long long* d_counters = nullptr;  // takes from the pools: per group, never reset
@@ -205,6 +206,7 @@ void release(phub_job* j) {
     if (j->d_tile_begin) (void)hipFree(j->d_tile_begin);
     if (j->d_tiles) (void)hipFree(j->d_tiles);
     if (j->d_rem_begin) (void)hipFree(j->d_rem_begin);
+    if (j->d_heads) (void)hipFree(j->d_heads);
     if (j->d_rems) (void)hipFree(j->d_rems);
     if (j->d_counters) (void)hipFree(j->d_counters);
     if (j->moments) (void)hipFree(j->moments);
@@ -372,6 +374,7 @@ int launch_group(phub_job* j, int g) {
         p.tile_begin = j->d_tile_begin + size_t(g) * (2 * size_t(j->bins) + 1);
         p.rems = j->d_rems;
         p.rem_begin = j->d_rem_begin + size_t(g) * (2 * size_t(j->bins) + 1);
+        p.heads = j->d_heads + size_t(g) * size_t(j->bins);
         p.grads = j->d_grads;
         p.outs = pull ? j->d_outs : nullptr;
         p.merge = j->merge;
@@ -481,6 +484,28 @@ int64_t append_device_tables(const Plan& plan, const std::vector<VirtualKey>& vk
         out->rem_begin.push_back(int32_t(out->rems.size()));
     }
     return elems;
+}
+
+void append_wave_heads(const DeviceTables& dt, size_t block, int bins,
+                       std::vector<WaveHead>* out) {
+    const int32_t* tb = dt.tile_begin.data() + block;
+    const int32_t* rb = dt.rem_begin.data() + block;
+    for (int w = 0; w < bins; ++w) {
+        WaveHead h{};
+        h.tiles_resident[0] = tb[w];
+        h.tiles_resident[1] = tb[w + 1];
+        h.tiles_streamed[0] = tb[bins + w];
+        h.tiles_streamed[1] = tb[bins + w + 1];
+        h.rems_resident[0] = rb[w];
+        h.rems_resident[1] = rb[w + 1];
+        h.rems_streamed[0] = rb[bins + w];
+        h.rems_streamed[1] = rb[bins + w + 1];
+        if (tb[w] < tb[w + 1]) h.first_resident = dt.tiles[size_t(tb[w])];
+        if (tb[bins + w] < tb[bins + w + 1]) h.first_streamed = dt.tiles[size_t(tb[bins + w])];
+        if (rb[w] < rb[w + 1]) h.first_rem_resident = dt.rems[size_t(rb[w])];
+        if (rb[bins + w] < rb[bins + w + 1]) h.first_rem_streamed = dt.rems[size_t(rb[bins + w])];
+        out->push_back(h);
+    }
 }
 
 }  // namespace phub
@@ -864,12 +889,16 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
         const std::vector<phub::DevRem>& drems = dt.rems;
         const std::vector<int32_t>& tile_begin = dt.tile_begin;
         const std::vector<int32_t>& rem_begin = dt.rem_begin;
+        std::vector<phub::WaveHead> heads;
+        for (int g = 0; g < j->num_rgroups; ++g)
+            phub::append_wave_heads(dt, size_t(g) * (2 * size_t(j->bins) + 1), j->bins, &heads);
         j->num_tiles = int64_t(dtiles.size());
         j->num_rems = int64_t(drems.size());
         const size_t tile_bytes = std::max<size_t>(dtiles.size(), 1) * sizeof(phub::DevTile);
         const size_t rem_bytes = std::max<size_t>(drems.size(), 1) * sizeof(phub::DevRem);
         const size_t tb_bytes = tile_begin.size() * sizeof(int32_t);
         const size_t rb_bytes = rem_begin.size() * sizeof(int32_t);
+        const size_t head_bytes = heads.size() * sizeof(phub::WaveHead);
         const size_t tab_bytes = j->grads.size() * sizeof(const float*);
         const size_t counter_bytes =
             size_t(j->num_rgroups) * kCountersPerGroup * sizeof(unsigned long long);
@@ -878,6 +907,7 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
             hipMalloc(&j->d_tile_begin, tb_bytes) != hipSuccess ||
             hipMalloc(&j->d_rems, rem_bytes) != hipSuccess ||
             hipMalloc(&j->d_rem_begin, rb_bytes) != hipSuccess ||
+            hipMalloc(&j->d_heads, head_bytes) != hipSuccess ||
             hipMalloc(&j->d_grads, tab_bytes) != hipSuccess ||
             hipMalloc(&j->d_outs, tab_bytes) != hipSuccess ||
             (j->dynamic && hipMalloc(&j->d_counters, counter_bytes) != hipSuccess)) {
@@ -900,6 +930,8 @@ int phub_init_ex(phub_job** out, int num_workers, int num_keys, const int64_t* k
                      "hipMemsetAsync(pool counters)");
         PHUB_TRY(hipMemcpy(j->d_rem_begin, rem_begin.data(), rb_bytes, hipMemcpyHostToDevice),
                  "hipMemcpy(remainder bins)");
+        PHUB_TRY(hipMemcpy(j->d_heads, heads.data(), head_bytes, hipMemcpyHostToDevice),
+                 "hipMemcpy(wave heads)");
         for (int i = 0; i < kStageSlots; ++i) {
             if (hipHostMalloc(reinterpret_cast<void**>(&j->stage[i]), tab_bytes,
                               hipHostMallocDefault) != hipSuccess ||

@@ -30,7 +30,8 @@
 #include "plan.hpp"
 
 // Largest schedule plus pointer table one call can hold: 4 MiB, enough for
-// about 250 M parameters in 1024-element tiles (16 bytes each) with the
+// about 240 M parameters in 1024-element tiles (16 bytes each, beside the
+// 128 KB of wave heads) with the
 // pointer table of thousands of (worker, key) pairs.
 #define PHUB_NOALLOC_SCRATCH_BYTES (size_t(4) << 20)
 
@@ -170,12 +171,20 @@ extern "C" int phub_step_noalloc(int num_workers, int num_keys, const int64_t* k
         return report_error(PHUB_ENOMEM, "host allocation failed while building the schedule");
     }
     if (dt.tiles.empty() && dt.rems.empty()) return PHUB_OK;  // every key is empty
+    std::vector<phub::WaveHead> heads;
+    try {
+        phub::append_wave_heads(dt, 0, bins, &heads);
+    } catch (const std::bad_alloc&) {
+        return report_error(PHUB_ENOMEM, "host allocation failed while building the schedule");
+    }
 
     // Scratch layout, each region 256-byte aligned: bin offsets of tiles and
-    // remainders, tiles, remainders, gradient pointer table (row = key).
+    // remainders, the waves' heads, tiles, remainders, gradient pointer
+    // table (row = key).
     const size_t off_tb = 0;
     const size_t off_rb = align_up(off_tb + dt.tile_begin.size() * sizeof(int32_t));
-    const size_t off_tiles = align_up(off_rb + dt.rem_begin.size() * sizeof(int32_t));
+    const size_t off_heads = align_up(off_rb + dt.rem_begin.size() * sizeof(int32_t));
+    const size_t off_tiles = align_up(off_heads + heads.size() * sizeof(phub::WaveHead));
     const size_t off_rems = align_up(off_tiles + dt.tiles.size() * sizeof(phub::DevTile));
     const size_t off_grads = align_up(off_rems + dt.rems.size() * sizeof(phub::DevRem));
     const size_t total = off_grads + table_bytes;
@@ -191,6 +200,7 @@ extern "C" int phub_step_noalloc(int num_workers, int num_keys, const int64_t* k
     }
     std::memcpy(host.data() + off_tb, dt.tile_begin.data(), dt.tile_begin.size() * sizeof(int32_t));
     std::memcpy(host.data() + off_rb, dt.rem_begin.data(), dt.rem_begin.size() * sizeof(int32_t));
+    std::memcpy(host.data() + off_heads, heads.data(), heads.size() * sizeof(phub::WaveHead));
     if (!dt.tiles.empty())
         std::memcpy(host.data() + off_tiles, dt.tiles.data(), dt.tiles.size() * sizeof(phub::DevTile));
     if (!dt.rems.empty())
@@ -216,6 +226,7 @@ extern "C" int phub_step_noalloc(int num_workers, int num_keys, const int64_t* k
     phub::StepParams p{};
     p.tile_begin = reinterpret_cast<const int32_t*>(setup.scratch + off_tb);
     p.rem_begin = reinterpret_cast<const int32_t*>(setup.scratch + off_rb);
+    p.heads = reinterpret_cast<const phub::WaveHead*>(setup.scratch + off_heads);
     p.tiles = reinterpret_cast<const phub::DevTile*>(setup.scratch + off_tiles);
     p.rems = reinterpret_cast<const phub::DevRem*>(setup.scratch + off_rems);
     p.grads = reinterpret_cast<const float* const*>(setup.scratch + off_grads);
