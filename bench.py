@@ -566,6 +566,11 @@ def main(argv=None) -> int:
                     help="ablation: chunks of --chunk-bytes are indivisible items of the "
                          "schedule, as in the paper (by default they are split while there are "
                          "fewer than 128 items per wave)")
+    ap.add_argument("--library", default=None,
+                    help="ablation: run the step from another build of the library, e.g. "
+                         "paper_1805_07891_amd/libphub_gradients_cached.so (gradients loaded "
+                         "cache-allocating; python -m paper_1805_07891_amd.build "
+                         "--gradients-cached builds it)")
     ap.add_argument("--resident-bytes", type=int, default=None,
                     help="per-job budget for keeping W and M in the memory-side cache "
                          "(library default if omitted)")
@@ -643,7 +648,7 @@ def main(argv=None) -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     dev = torch.device("cuda:0")
-    lib = load_library()
+    lib = load_library(os.path.abspath(args.library) if args.library else None)
 
     if args.streaming:
         return streaming_bench(torch, dev, lib, workloads.workload(args.workload or "resnet50"),
@@ -888,7 +893,8 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
     dom = max(range(len(jobs)), key=lambda j: job_bytes(wl.jobs[j]))
     traffic = (None if (args.pushpull or args.unfused or args.optimizer != "momentum" or
                         args.resident_bytes is not None or args.shared_stream or args.cu_masks or
-                        args.whole_chunks or args.schedule != "lpt" or args.chunk_bytes)
+                        args.whole_chunks or args.schedule != "lpt" or args.chunk_bytes or
+                        args.library)
                else measured_traffic(wl.name))
     groups, threads, segs, _, _ = jobs[dom].info()
     cached = [job.cached_fraction() for job in jobs]
@@ -939,6 +945,7 @@ def measure(torch, dev, lib, wl, args, cpu_seconds: float, streams, helper) -> d
             "pushpull": args.pushpull,
             "optimizer_kind": args.optimizer,
             "unfused": args.unfused,
+            "library": args.library or "paper_1805_07891_amd/libphub.so",
             "streams": ("one shared by the jobs" if shared_stream else
                         "one per job, CU-masked" if masked is not None else
                         "one per job" if len(wl.jobs) > 1 else "one"),

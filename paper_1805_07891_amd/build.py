@@ -20,6 +20,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libphub.so")
 PROBE_LIB = os.path.join(PKG, "libphub_probe.so")
+# Ablation build: the gradients loaded cache-allocating (run it with
+# bench.py --library); not built by default.
+GRADIENTS_CACHED_LIB = os.path.join(PKG, "libphub_gradients_cached.so")
 PROBE_SOURCES = ["probe.hip"]
 
 SOURCES = ["plan.cpp", "phub_api.cpp", "fused_step.hip", "step_noalloc.hip"]
@@ -84,6 +87,15 @@ def build_all(verbose: bool = False) -> None:
     build_probe(verbose=verbose)
 
 
+def build_gradients_cached(verbose: bool = False) -> str:
+    """The ablation library whose kernels load the gradients
+    cache-allocating (PHUB_GRADIENT_LOADS_CACHED) instead of non-temporally."""
+    return build(GRADIENTS_CACHED_LIB, defines=["PHUB_GRADIENT_LOADS_CACHED=1"], verbose=verbose)
+
+
 if __name__ == "__main__":
-    build_all(verbose=True)
+    if "--gradients-cached" in sys.argv[1:]:
+        build_gradients_cached(verbose=True)
+    else:
+        build_all(verbose=True)
     sys.exit(0)

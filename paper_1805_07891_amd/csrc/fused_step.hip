@@ -151,9 +151,20 @@ __device__ __forceinline__ void update4(const f4& s, f4* st, OptArgs o) {
 #define PHUB_GLOBAL __attribute__((address_space(1)))
 #define PHUB_LDS __attribute__((address_space(3)))
 
+// Gradient loads (and the unfused variant's sum buffer): non-temporal, as
+// each gradient byte is read once.  A build with PHUB_GRADIENT_LOADS_CACHED
+// set loads them cache-allocating instead: the ablation of caching the
+// gradients beside the model (the paper's Table 4).
+#ifndef PHUB_GRADIENT_LOADS_CACHED
+#define PHUB_GRADIENT_LOADS_CACHED 0
+#endif
 __device__ __forceinline__ f4 load_stream(const float* base, uint32_t byte_off) {
     const PHUB_GLOBAL char* b = (const PHUB_GLOBAL char*)base;
+#if PHUB_GRADIENT_LOADS_CACHED
+    return *(const PHUB_GLOBAL f4*)(b + byte_off);
+#else
     return __builtin_nontemporal_load((const PHUB_GLOBAL f4*)(b + byte_off));
+#endif
 }
 
 // State accesses.  The policy is a template argument resolved with
