@@ -20,20 +20,21 @@
 // write streams (the state); on MI355X such a mix reaches the highest
 // bandwidth with few waves per CU.
 //
-// Memory access: a wave walks its full tiles, then its remainders.  A tile
-// is 1024 elements of each of the N + S arrays: a lane takes 4 float4 of
-// each (the wave's 64 lanes cover 4 contiguous 1 KB pieces).  Segments are
-// cut on the host into full tiles and a remainder, so the tile loop is
+// Memory access: a wave reads its head (its bins and the first descriptor
+// of each, WaveHead), then walks its full tiles, then its remainders.  A
+// tile is 1024 elements of each of the N + S arrays: a lane takes 4 float4
+// of each (the wave's 64 lanes cover 4 contiguous 1 KB pieces).  Segments
+// are cut on the host into full tiles and a remainder, so the tile loop is
 // straight-line code.  The tile's loads go out piece by piece in a sliding
 // window that continues into the wave's next tile (see the load window
 // below); each piece is optimized as soon as its last gradient is in, and
 // written back at once, or, from enough gradient streams per state stream,
 // in bursts of several tiles through LDS, timed by a chip-wide clock so
-// that all waves write together (the burst write-back below).  Gradients are read once per step and loaded
-// non-temporally.  A wave has two bins: the part of the job whose state is
-// read and written non-temporally like the gradients, and the part whose
-// state stays in the memory-side cache between steps (cache-allocating
-// loads and stores).  Either may be empty.
+// that all waves write together (the burst write-back below).  Gradients
+// are read once per step and loaded non-temporally.  A wave has two bins:
+// the part of the job whose state is read and written non-temporally like
+// the gradients, and the part whose state stays in the memory-side cache
+// between steps (cache-allocating loads and stores).  Either may be empty.
 //
 // Arithmetic (no MFMA: the work is elementwise and HBM-bound): the sum is a
 // left fold in ascending worker index, plain fp32 additions; then the
