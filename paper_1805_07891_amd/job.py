@@ -87,10 +87,16 @@ class TorchJob:
         # every worker's key pointers in one table (worker-major) for phub_push_all
         self._all_ptrs = (ctypes.c_void_p * (spec.num_workers * spec.num_keys))()
         self._attached = 0
-        # the two calls of every step, bound once (a step of a small job costs a
-        # few microseconds, and each layer of Python adds to it)
-        self._raw_push_all = self.lib.lib.phub_push_all
-        self._raw_step = self.lib.lib.phub_step
+        # the two calls of every step, bound once and without ctypes argument
+        # conversion (their arguments are prepared ctypes objects): a step of
+        # a small job costs a few microseconds, and each layer of Python adds
+        # to it (the conversion about 0.1-0.2 us per call)
+        dll = self.lib.lib
+        self._raw_push_all = dll._FuncPtr(("phub_push_all", dll))
+        self._raw_push_all.restype = ctypes.c_int
+        self._raw_step = dll._FuncPtr(("phub_step", dll))
+        self._raw_step.restype = ctypes.c_int
+        self._handle_arg = ctypes.c_void_p(self.handle)
 
     # -- inputs ----------------------------------------------------------------
     def key_pointers(self, arena) -> List[int]:
@@ -126,7 +132,7 @@ class TorchJob:
         if self._attached != self.spec.num_workers:
             missing = [w for w, a in enumerate(self._ptr_arrays) if a is None]
             raise RuntimeError(f"workers {missing} have no gradient arena attached")
-        rc = self._raw_push_all(self.handle, self._all_ptrs)
+        rc = self._raw_push_all(self._handle_arg, self._all_ptrs)
         if rc:
             self.lib._check(rc, True)
 
@@ -172,7 +178,7 @@ class TorchJob:
             self.lib.phub_pushpull_keys(self.handle, w, arr, self._model_ptrs[w])
 
     def step(self) -> None:
-        rc = self._raw_step(self.handle)
+        rc = self._raw_step(self._handle_arg)
         if rc:
             self.lib._check(rc, True)
 
@@ -259,6 +265,7 @@ class TorchJob:
         if self.handle is not None:
             self.lib.phub_destroy(self.handle)
             self.handle = None
+            self._handle_arg = ctypes.c_void_p(None)
 
     def __del__(self):
         try:
