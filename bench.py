@@ -92,7 +92,8 @@ def measured_traffic(workload: str):
 NOTES = {
     "tiny": "cache-resident and launch-bound: 26.5 MB per step (3.3 us at peak) fits in the "
             "256 MiB memory-side cache, and back-to-back kernels on one stream start about "
-            "0.95 us apart on MI355X; host_us_per_step is the push and step calls",
+            "0.95 us apart on MI355X; host_us_per_step is the time in the push and step "
+            "calls, which over many steps includes waiting for a full launch queue",
 }
 
 
